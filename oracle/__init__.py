@@ -1,0 +1,46 @@
+"""CPU oracle for draft-step attention over reused target KV -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline``
+leg may import or call anything in this package.  The product path (the HIP
+library and its Python binding) never imports it and shares no code with it.
+
+What it computes (KVShot, arXiv 2604.26412):
+  * a drafter query re-attends the target's un-aggregated K/V with its own
+    query (Sec. 2.2, Eq. 2);
+  * the cross-attention memory of a draft step is the target KV of the verified
+    prefix plus the drafter's own KV for later draft positions, laid out like
+    an ordinary autoregressive KV cache (Sec. 3.4.1, Eq. 7; App. B,
+    "Cross-attention memory");
+  * draft tokens may be organised as a tree (Sec. 3.5, tree shape (8, 10, 60)).
+
+The method reaches plain masked softmax attention exactly, so the oracle is
+that definition written out in float64 NumPy, with explicit masks and its own
+page gather.  Conventions the paper leaves open (softmax scale, RoPE variant,
+draft positions, diagonal inclusivity, tree semantics, GQA mapping) are fixed
+by the readings listed in each function's docstring.
+
+Parity status per function:
+  * ``masked_attention``        -- pinned (closed forms, brute force, SDPA reduction)
+  * ``gather_prefix``           -- pinned (scatter/gather round trip, bit-exact)
+  * ``rope``                    -- pinned for internal consistency (identity at 0,
+                                   norm, relative position, complex form); the
+                                   choice of the rotate-half variant itself is a
+                                   convention: parity unpinned against the paper
+  * ``tree_ancestry``           -- pinned (chain == causal, star == self, brute walk)
+  * ``draft_attention_step`` / ``draft_attention_tree`` -- pinned through the
+    above plus step-by-step == folded and page-permutation invariance; the
+    softmax scale (1/sqrt(D)) and GQA head mapping are conventions:
+    parity unpinned against the paper.
+"""
+from .attention import (  # noqa: F401
+    decode,
+    gather_prefix,
+    rope,
+    rope_inv_freq,
+    masked_attention,
+    tree_ancestry,
+    draft_attention_step,
+    draft_attention_tree,
+    draft_attention,
+    gather_dense,
+)

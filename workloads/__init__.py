@@ -1,0 +1,304 @@
+"""Seeded synthetic inputs for draft-step attention over reused target KV.
+
+This module only *makes inputs*: random tensors, their bf16 encoding, page
+tables, ragged lengths, step offsets and draft-tree parent arrays.  It holds
+none of the attention arithmetic.  Both the CPU oracle (via the tests) and the
+HIP path are fed the very same bit patterns produced here.
+
+Recipe (all values N(0, 1) unless stated):
+  * generator: ``numpy.random.Generator(PCG64(SeedSequence([seed, tensor_id])))``;
+    float32 samples are rounded to bf16 with round-to-nearest-even on the bits;
+  * target K/V are generated per sequence in logical token order and then
+    scattered into physical pages, so the logical data does not depend on the
+    page table;
+  * pages are HND: ``pages[page][kv_head][slot][head_dim]``;
+  * the page pool has ~1% spare pages; spare pages and unused tail slots are
+    filled with NaN, and page-table padding is -1 (poisoning: a kernel that
+    reads them, or multiplies a masked weight by them, produces NaN);
+  * outlier channels (optional): for each KV head, ``n_outlier`` distinct
+    channels of the target *keys* are multiplied by ``outlier_scale`` before
+    rounding;
+  * draft trees: node 0 is the only root, and node i > 0 picks its parent
+    uniformly among earlier nodes with depth <= max_depth - 2 and fewer than
+    ``max_branch`` children (so depth index <= max_depth - 1).
+
+The shapes follow the Qwen3-8B attention geometry the paper's target model
+uses (32 query heads, 8 KV heads, head_dim 128).  They are synthetic stand-ins:
+no dataset, no trained weights.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+BF16_NAN = np.uint16(0x7FC0)
+
+# tensor ids inside one seed's stream family
+_TID_Q = 1
+_TID_DK = 2
+_TID_DV = 3
+_TID_PERM = 4
+_TID_LENS = 5
+_TID_OFFS = 6
+_TID_OUTLIER = 7
+_TID_K = 1000   # + b
+_TID_V = 2000   # + b
+_TID_TREE = 3000  # + b
+
+
+def rng_for(seed: int, tensor_id: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(seed), int(tensor_id)])))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (round-to-nearest-even) and return the raw uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    bias = np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))
+    bits = ((u + bias) >> np.uint64(16)).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        bits[nan] = BF16_NAN
+    return bits
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bits to float32 (test convenience; not used by the oracle)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal(seed: int, tid: int, shape, chunk: int = 1 << 24) -> np.ndarray:
+    g = rng_for(seed, tid)
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.float32)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        out[s:e] = g.standard_normal(e - s, dtype=np.float32)
+    return out.reshape(shape)
+
+
+def _encode(x: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x)
+    if dtype == "fp32":
+        return np.ascontiguousarray(x, dtype=np.float32)
+    raise ValueError(dtype)
+
+
+def _nan_fill(dtype: str):
+    return BF16_NAN if dtype == "bf16" else np.float32(np.nan)
+
+
+def random_tree(seed: int, b: int, n_nodes: int, max_depth: int = 8, max_branch: int = 4) -> np.ndarray:
+    """Parent array of one seeded random draft tree (node 0 is the root, parents[i] < i)."""
+    g = rng_for(seed, _TID_TREE + b)
+    parents = np.full(n_nodes, -1, dtype=np.int32)
+    depth = np.zeros(n_nodes, dtype=np.int32)
+    children = np.zeros(n_nodes, dtype=np.int32)
+    for i in range(1, n_nodes):
+        cand = [j for j in range(i) if depth[j] <= max_depth - 2 and children[j] < max_branch]
+        if not cand:
+            raise ValueError("tree capacity exhausted")
+        p = cand[int(g.integers(len(cand)))]
+        parents[i] = p
+        depth[i] = depth[p] + 1
+        children[p] += 1
+    return parents
+
+
+@dataclass
+class DraftCase:
+    """One draft-attention call's inputs (host arrays) plus its static geometry."""
+    mode: str                      # "step" or "tree"
+    dtype: str                     # "bf16" (uint16 bit patterns) or "fp32"
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    max_draft: int
+    n_new: int                     # queries per sequence (draft steps, or tree nodes)
+    q: np.ndarray                  # [B][n_new][Hq][D]
+    k_pages: np.ndarray            # [num_pages][Hkv][P][D]
+    v_pages: np.ndarray
+    page_table: np.ndarray         # int32 [B][max_pages_per_seq], padding -1
+    ctx_lens: np.ndarray           # int32 [B]
+    draft_k: np.ndarray            # [B][max_draft][Hkv][D]  (pre-RoPE)
+    draft_v: np.ndarray
+    step_offsets: Optional[np.ndarray] = None   # int32 [B] (step mode)
+    parents: Optional[np.ndarray] = None        # int32 [B][n_new] (tree mode)
+    rope_theta: float = 1e6
+    softmax_scale: float = 0.0                  # 0 -> 1/sqrt(head_dim)
+    seed: int = 0
+    name: str = ""
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def batch(self) -> int:
+        return int(self.q.shape[0])
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.k_pages.shape[0])
+
+    @property
+    def max_pages_per_seq(self) -> int:
+        return int(self.page_table.shape[1])
+
+    @property
+    def scale(self) -> float:
+        return self.softmax_scale if self.softmax_scale != 0.0 else 1.0 / float(np.sqrt(self.head_dim))
+
+    def draft_len(self, b: int) -> int:
+        """Number of draft keys sequence b's queries can see in total."""
+        if self.mode == "step":
+            return int(self.step_offsets[b]) + self.n_new
+        return self.n_new
+
+
+def build_pages(seed: int, ctx_lens: Sequence[int], num_kv_heads: int, head_dim: int, page_size: int,
+                dtype: str, *, shuffle: bool = True, spare_frac: float = 0.01, poison: bool = True,
+                n_outlier: int = 0, outlier_scale: float = 8.0, min_pages_per_seq: int = 1,
+                max_pages_per_seq: Optional[int] = None):
+    """Target K/V pools, page table and per-sequence logical K/V (float32, pre-rounding ignored).
+
+    Returns (k_pages, v_pages, page_table).
+    """
+    B = len(ctx_lens)
+    npages = [max(min_pages_per_seq, -(-int(t) // page_size)) if t > 0 else 0 for t in ctx_lens]
+    used = int(sum(npages))
+    spare = max(1, int(np.ceil(used * spare_frac)))
+    pool = used + spare
+    mpps = max_pages_per_seq if max_pages_per_seq is not None else max(1, max(npages) if npages else 1)
+    if mpps < max(npages):
+        raise ValueError("max_pages_per_seq too small")
+    perm = rng_for(seed, _TID_PERM).permutation(pool).astype(np.int32) if shuffle \
+        else np.arange(pool, dtype=np.int32)
+    edt = np.uint16 if dtype == "bf16" else np.float32
+    fill = _nan_fill(dtype) if poison else edt(0)
+    k_pages = np.full((pool, num_kv_heads, page_size, head_dim), fill, dtype=edt)
+    v_pages = np.full((pool, num_kv_heads, page_size, head_dim), fill, dtype=edt)
+    page_table = np.full((B, mpps), -1, dtype=np.int32)
+    outl = None
+    if n_outlier > 0:
+        g = rng_for(seed, _TID_OUTLIER)
+        outl = np.stack([g.choice(head_dim, size=n_outlier, replace=False) for _ in range(num_kv_heads)])
+    cursor = 0
+    for b, T in enumerate(ctx_lens):
+        T = int(T)
+        if npages[b] == 0:
+            continue
+        ids = perm[cursor:cursor + npages[b]]
+        cursor += npages[b]
+        page_table[b, :npages[b]] = ids
+        if T == 0:
+            continue
+        K = _normal(seed, _TID_K + b, (T, num_kv_heads, head_dim))
+        V = _normal(seed, _TID_V + b, (T, num_kv_heads, head_dim))
+        if outl is not None:
+            for h in range(num_kv_heads):
+                K[:, h, outl[h]] *= np.float32(outlier_scale)
+        Ke = _encode(K, dtype)
+        Ve = _encode(V, dtype)
+        t = np.arange(T)
+        k_pages[ids[t // page_size], :, t % page_size, :] = Ke
+        v_pages[ids[t // page_size], :, t % page_size, :] = Ve
+    return k_pages, v_pages, page_table
+
+
+def make_case(*, mode: str = "step", batch: int = 1, ctx_lens=None, n_new: int = 4,
+              num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128, page_size: int = 16,
+              dtype: str = "bf16", seed: int = 0, max_draft: Optional[int] = None, step_offsets=None,
+              parents=None, shuffle: bool = True, poison: bool = True, n_outlier: int = 0,
+              rope_theta: float = 1e6, softmax_scale: float = 0.0, name: str = "",
+              max_pages_per_seq: Optional[int] = None) -> DraftCase:
+    if ctx_lens is None:
+        ctx_lens = [256] * batch
+    ctx_lens = np.asarray(ctx_lens, dtype=np.int32)
+    B = len(ctx_lens)
+    if mode == "step":
+        if step_offsets is None:
+            step_offsets = np.zeros(B, dtype=np.int32)
+        step_offsets = np.asarray(step_offsets, dtype=np.int32)
+        need = int((step_offsets + n_new).max())
+    else:
+        if parents is None:
+            parents = np.stack([random_tree(seed, b, n_new) for b in range(B)])
+        parents = np.asarray(parents, dtype=np.int32)
+        need = n_new
+    if max_draft is None:
+        max_draft = need
+    if max_draft < need:
+        raise ValueError("max_draft too small")
+    k_pages, v_pages, page_table = build_pages(seed, ctx_lens, num_kv_heads, head_dim, page_size, dtype,
+                                               shuffle=shuffle, poison=poison, n_outlier=n_outlier,
+                                               max_pages_per_seq=max_pages_per_seq)
+    q = _encode(_normal(seed, _TID_Q, (B, n_new, num_q_heads, head_dim)), dtype)
+    dk = _encode(_normal(seed, _TID_DK, (B, max_draft, num_kv_heads, head_dim)), dtype)
+    dv = _encode(_normal(seed, _TID_DV, (B, max_draft, num_kv_heads, head_dim)), dtype)
+    if poison:
+        # draft slots no query can see are poison too
+        for b in range(B):
+            s_len = int(step_offsets[b]) + n_new if mode == "step" else n_new
+            dk[b, s_len:] = _nan_fill(dtype)
+            dv[b, s_len:] = _nan_fill(dtype)
+    return DraftCase(mode=mode, dtype=dtype, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                     head_dim=head_dim, page_size=page_size, max_draft=max_draft, n_new=n_new, q=q,
+                     k_pages=k_pages, v_pages=v_pages, page_table=page_table, ctx_lens=ctx_lens,
+                     draft_k=dk, draft_v=dv, step_offsets=step_offsets if mode == "step" else None,
+                     parents=parents if mode == "tree" else None, rope_theta=rope_theta,
+                     softmax_scale=softmax_scale, seed=seed, name=name)
+
+
+# ---------------------------------------------------------------------------
+# The five workload shapes (Qwen3-8B-shaped synthetic stand-ins).
+# ---------------------------------------------------------------------------
+
+def ragged_lengths(seed: int, batch: int, lo: int, hi: int) -> np.ndarray:
+    return rng_for(seed, _TID_LENS).integers(lo, hi + 1, size=batch).astype(np.int32)
+
+
+def ragged_offsets(seed: int, batch: int, hi: int) -> np.ndarray:
+    return rng_for(seed, _TID_OFFS).integers(0, hi + 1, size=batch).astype(np.int32)
+
+
+WORKLOADS = {
+    # tiny fp32 case: batch 1, ctx 256, k=4 causal draft steps, one contiguous 256-token page
+    "tiny_fp32_ctx256": dict(mode="step", ctx_lens=[256], n_new=4, dtype="fp32", page_size=256,
+                             shuffle=False, seed=1001),
+    # one Qwen3-8B-shaped sequence, ctx 4096, k=8, outlier key channels, shuffled 16-token pages
+    "single_ctx4096_k8": dict(mode="step", ctx_lens=[4096], n_new=8, dtype="bf16", page_size=16,
+                              n_outlier=4, seed=1002),
+    # ragged batch of 16, ctx ~ U[512, 8192], k=6, per-sequence step offsets U{0..8}
+    "ragged_b16_k6": dict(mode="step", n_new=6, dtype="bf16", page_size=16, seed=1003, max_draft=16),
+    # long range: batch 64 x ctx 32768, k=8 (too large for host generation in tests)
+    "long_b64_ctx32k_k8": dict(mode="step", ctx_lens=[32768] * 64, n_new=8, dtype="bf16", page_size=16,
+                               seed=1004),
+    # draft tree: batch 8 x ctx 16384, 60-node tree (depth <= 8, branching <= 4)
+    "tree_b8_ctx16k_n60": dict(mode="tree", ctx_lens=[16384] * 8, n_new=60, dtype="bf16", page_size=16,
+                               seed=1005),
+}
+
+
+def workload(name: str, **overrides) -> DraftCase:
+    spec = dict(WORKLOADS[name])
+    spec.update(overrides)
+    if name.startswith("ragged") and "ctx_lens" not in overrides:
+        spec["ctx_lens"] = ragged_lengths(spec["seed"], 16, 512, 8192)
+        spec["step_offsets"] = ragged_offsets(spec["seed"], 16, 8)
+    return make_case(name=name, **spec)
+
+
+def algorithmic_bytes(case_or_dims, *, elem_bytes: int = 2) -> int:
+    """Unique bytes one call must move: target K+V once, q, draft K/V seen, page-table entries, output."""
+    c = case_or_dims
+    D, Hkv, Hq, P = c.head_dim, c.num_kv_heads, c.num_q_heads, c.page_size
+    tot = 0
+    for b in range(c.batch):
+        T = int(c.ctx_lens[b])
+        tot += 2 * T * Hkv * D * elem_bytes
+        tot += -(-T // P) * 4
+        tot += 2 * c.draft_len(b) * Hkv * D * elem_bytes
+    tot += 2 * c.batch * c.n_new * Hq * D * elem_bytes  # q in, out
+    return tot
