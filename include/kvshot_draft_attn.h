@@ -1,0 +1,175 @@
+/*
+ * kvshot_draft_attn.h -- C ABI of the draft-step attention library for MI355X (gfx950).
+ *
+ * Operation (KVShot, arXiv 2604.26412):
+ *   A drafter query re-attends the target model's un-aggregated per-token K/V
+ *   with its own query (Sec. 2.2, Eq. 2).  The memory a draft step attends is
+ *   the target KV of the verified prefix followed by the drafter's own KV for
+ *   later draft positions, as in an ordinary autoregressive KV cache
+ *   (Sec. 3.4.1, Eq. 7; App. B, "Cross-attention memory").  Draft tokens are a
+ *   linear chain of steps or a tree (Sec. 3.5, tree (8, 10, 60)).
+ *
+ *   For sequence b with T_b prefix tokens, query head hq (KV head hq / G,
+ *   G = num_q_heads / num_kv_heads) and query row j:
+ *     out = sum_{allowed keys} softmax(scale * <rope(q, pos_j), key>) * value
+ *   where the keys are the T_b target keys (stored already rotated, used as
+ *   is) followed by the draft keys, each rotated at its own position, and
+ *     step mode: query j sits at draft step s0 + j (s0 = step_offsets[b]),
+ *                position T_b + s0 + j; draft key s sits at position T_b + s
+ *                and is visible to query j iff s <= s0 + j;
+ *     tree mode: node i sits at position T_b + depth(i); draft key s is node s's
+ *                key at T_b + depth(s), visible to node i iff s is i or one of
+ *                its ancestors (parents[i] == -1 marks a root).
+ *   RoPE is rotate-half: channel m pairs with m + D/2, angle pos * theta^(-2m/D).
+ *   scale defaults to 1/sqrt(head_dim).
+ *
+ * Conventions for every call:
+ *   - Every array pointer is a DEVICE pointer unless marked (host).
+ *   - bf16 data is passed as raw 16-bit patterns; fp32 as IEEE float.
+ *   - The caller owns every array and keeps it alive until the work queued on
+ *     `stream` (a hipStream_t, NULL = default stream) has finished.
+ *   - Functions never throw or abort.  Argument errors found on the host are
+ *     returned before anything is queued and leave `out` untouched.  Queued
+ *     work performs no host synchronisation (except validate, which does).
+ *   - Data-dependent contract violations (a page id outside the pool, a length
+ *     above the hint, a bad parent) never make a kernel read out of bounds:
+ *     indices are clamped.  The result is then unspecified; call
+ *     kvshot_draft_attn_validate to detect them.
+ *   - A handle may be used by one stream at a time.
+ */
+#ifndef KVSHOT_DRAFT_ATTN_H
+#define KVSHOT_DRAFT_ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KVSHOT_OK = 0,
+  KVSHOT_ERR_INVALID_ARG = 1,   /* null pointer, size out of range, inconsistent config */
+  KVSHOT_ERR_UNSUPPORTED = 2,   /* valid but not implemented (head_dim != 128, ...) */
+  KVSHOT_ERR_OUT_OF_MEMORY = 3, /* device allocation in init failed */
+  KVSHOT_ERR_DEVICE = 4,        /* a HIP call or kernel launch failed */
+  KVSHOT_ERR_DATA = 5           /* validate found a contract violation in device data */
+} kvshot_status;
+
+typedef enum { KVSHOT_BF16 = 0, KVSHOT_FP32 = 1 } kvshot_dtype;
+
+typedef struct kvshot_config {
+  int32_t num_q_heads;        /* Hq; Hq % Hkv == 0 and G = Hq / Hkv <= 8 */
+  int32_t num_kv_heads;       /* Hkv >= 1 */
+  int32_t head_dim;           /* D; must be 128 */
+  int32_t page_size;          /* P; power of two in [16, 256] */
+  int32_t dtype;              /* kvshot_dtype of q, K/V pages and draft K/V */
+  int32_t out_dtype;          /* kvshot_dtype of out */
+  int32_t max_batch;          /* largest batch any call will pass */
+  int32_t max_draft;          /* rows of the draft K/V arrays per sequence; 1..64 */
+  int32_t max_pages_per_seq;  /* row stride (entries) of page_table */
+  int32_t num_pages;          /* pages in the K (and V) pool; page ids are clamped to it */
+  int64_t max_position;       /* positions 0..max_position-1 get a RoPE table entry */
+  double rope_theta;          /* RoPE base, > 0 (1e6 for Qwen3) */
+  float softmax_scale;        /* 0 -> 1/sqrt(head_dim) */
+  int32_t reserved;           /* must be 0 */
+  int64_t page_stride;        /* elements between pages; 0 -> Hkv * P * D */
+  int64_t head_stride;        /* elements between KV heads in a page; 0 -> P * D */
+  int64_t slot_stride;        /* elements between slots in a page; 0 -> D.  head_dim is contiguous. */
+} kvshot_config;
+
+typedef struct kvshot_ctx* kvshot_handle;
+
+/* Validates `cfg`, selects the current HIP device, allocates the split-K
+ * workspace and builds the RoPE cos/sin table (float64 on the host, rounded to
+ * float32).  On success *out receives a handle.  Host pointers. */
+kvshot_status kvshot_draft_attn_init(const kvshot_config* cfg, kvshot_handle* out);
+
+/* Releases the handle's device memory (synchronises the device).  NULL is a no-op. */
+kvshot_status kvshot_draft_attn_destroy(kvshot_handle h);
+
+/* Step mode: n_new causal draft steps per sequence folded into one call.
+ *   q            [batch][n_new][Hq][D]  pre-RoPE draft queries
+ *   k_pages      target keys (already rotated), v_pages target values: element
+ *                (page, kv_head, slot, d) at page*page_stride + kv_head*head_stride
+ *                + slot*slot_stride + d
+ *   page_table   int32 [batch][max_pages_per_seq]; token t of sequence b is in
+ *                slot t % P of page page_table[b][t / P]; entries at or past
+ *                ceil(ctx_lens[b] / P) are never read
+ *   ctx_lens     int32 [batch]; 0 <= T_b <= max_ctx_len_hint
+ *   draft_k/v    [batch][max_draft][Hkv][D]; draft_k pre-RoPE; rows
+ *                [0, step_offsets[b] + n_new) are read
+ *   step_offsets int32 [batch]; 0 <= s0 and s0 + n_new <= max_draft
+ *   out          [batch][n_new][Hq][D] in out_dtype
+ *   lse          nullable float32 [batch][n_new][Hq], natural-log sum of exp of scores
+ *   max_ctx_len_hint (host) bounds T_b and sizes the split-K grid.
+ * Requirements: 1 <= batch <= max_batch, 1 <= n_new <= max_draft,
+ * G * n_new <= 256, max_ctx_len_hint <= max_pages_per_seq * P and
+ * max_ctx_len_hint + max_draft <= max_position. */
+kvshot_status kvshot_draft_attn_step(kvshot_handle h, int32_t batch, int32_t n_new, int32_t max_ctx_len_hint,
+                                     const void* q, const void* k_pages, const void* v_pages,
+                                     const int32_t* page_table, const int32_t* ctx_lens,
+                                     const void* draft_k, const void* draft_v, const int32_t* step_offsets,
+                                     void* out, float* lse, void* stream);
+
+/* Tree mode: n_nodes draft-tree nodes per sequence.
+ *   q            [batch][n_nodes][Hq][D]  pre-RoPE, node order
+ *   draft_k/v    [batch][max_draft][Hkv][D]; row i is node i's key/value
+ *   parents      int32 [batch][n_nodes]; parents[b][i] in {-1} U [0, i)
+ * Other arguments as in kvshot_draft_attn_step; 1 <= n_nodes <= max_draft. */
+kvshot_status kvshot_draft_attn_tree(kvshot_handle h, int32_t batch, int32_t n_nodes, int32_t max_ctx_len_hint,
+                                     const void* q, const void* k_pages, const void* v_pages,
+                                     const int32_t* page_table, const int32_t* ctx_lens,
+                                     const void* draft_k, const void* draft_v, const int32_t* parents,
+                                     void* out, float* lse, void* stream);
+
+/* Checks device-side contract data for a call with these sizes: every page id a
+ * call would read lies in [0, num_pages), 0 <= ctx_lens[b] <= max_ctx_len_hint,
+ * step offsets in range (if step_offsets != NULL), parents in {-1} U [0, i)
+ * (if parents != NULL).  Synchronises `stream`.  Returns KVSHOT_OK or
+ * KVSHOT_ERR_DATA; *first_bad (host, nullable) receives a code naming the
+ * first kind of violation found (0 none, 1 ctx_len, 2 page id, 3 step offset,
+ * 4 parent). */
+kvshot_status kvshot_draft_attn_validate(kvshot_handle h, int32_t batch, int32_t n_queries, int32_t max_ctx_len_hint,
+                                         const int32_t* page_table, const int32_t* ctx_lens,
+                                         const int32_t* step_offsets, const int32_t* parents,
+                                         int32_t* first_bad, void* stream);
+
+/* Tuning and introspection. */
+typedef enum {
+  KVSHOT_OPT_SPLITS = 0,   /* value 0: automatic split-K count; n > 0: use n (clamped to the workspace) */
+  KVSHOT_OPT_PATH = 1,     /* 0 automatic, 1 MFMA kernel (bf16 only), 2 generic VALU kernel */
+  KVSHOT_OPT_PROFILE = 2   /* 1: record HIP events around the attention and combine kernels of every call */
+} kvshot_option;
+kvshot_status kvshot_draft_attn_set_option(kvshot_handle h, int32_t option, int64_t value);
+
+/* Plan a call would use: split count, path (1 MFMA, 2 generic), 32-row query tiles,
+ * and grid size in workgroups of the attention kernel.  Host outputs, each nullable. */
+kvshot_status kvshot_draft_attn_plan(kvshot_handle h, int32_t batch, int32_t n_queries, int32_t max_ctx_len_hint,
+                                     int32_t* splits, int32_t* path, int32_t* row_tiles, int32_t* workgroups);
+
+/* With KVSHOT_OPT_PROFILE on: synchronises, then returns the summed event time
+ * (ms) of the attention kernel and of the combine kernel over the calls since
+ * the last read, and the call count; resets the sums.  Host outputs. */
+kvshot_status kvshot_draft_attn_profile_read(kvshot_handle h, double* attn_ms, double* combine_ms, int64_t* calls);
+
+/* Debug: the dense logical view [batch][max_ctx][Hkv][D] (dtype of the pools)
+ * of the paged target K/V, produced by the same page-addressing code the
+ * attention kernels use.  Positions >= ctx_lens[b] are written as zero. */
+kvshot_status kvshot_debug_gather_kv(kvshot_handle h, int32_t batch, int32_t max_ctx, const void* k_pages,
+                                     const void* v_pages, const int32_t* page_table, const int32_t* ctx_lens,
+                                     void* k_dense, void* v_dense, void* stream);
+
+/* Debug: ancestor-or-self bitmasks (bit s of anc_out[b][i] set iff node s is i or
+ * an ancestor of i) and depths of the draft trees, produced by the same code the
+ * tree kernels use.  anc_out uint64 [batch][n_nodes], depth_out int32 [batch][n_nodes]. */
+kvshot_status kvshot_debug_tree_mask(kvshot_handle h, int32_t batch, int32_t n_nodes, const int32_t* parents,
+                                     uint64_t* anc_out, int32_t* depth_out, void* stream);
+
+/* Static text for a status code. */
+const char* kvshot_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVSHOT_DRAFT_ATTN_H */

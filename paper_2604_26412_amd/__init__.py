@@ -1,0 +1,283 @@
+"""Draft-step attention over reused target KV on MI355X (gfx950): Python binding.
+
+Thin ctypes layer over ``libkvshot_draft_attn.so`` (C ABI in
+``include/kvshot_draft_attn.h``).  It only marshals arguments: it checks
+tensor dtypes, shapes, devices and contiguity, takes ``data_ptr()`` and the
+current HIP stream from PyTorch, and calls the library.  Every step of the
+computation runs in the library's HIP kernels; there is no fallback.  If the
+library is missing, importing works but the first use raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = ["DraftAttention", "KvshotError", "load_library", "LIB_PATH", "EXPORTED_SYMBOLS"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
+
+KVSHOT_OK = 0
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_MEMORY", 4: "DEVICE", 5: "DATA"}
+BF16, FP32 = 0, 1
+OPT_SPLITS, OPT_PATH, OPT_PROFILE = 0, 1, 2
+
+EXPORTED_SYMBOLS = [
+    "kvshot_draft_attn_init", "kvshot_draft_attn_destroy", "kvshot_draft_attn_step", "kvshot_draft_attn_tree",
+    "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
+    "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_status_string",
+]
+
+
+class KvshotConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32), ("max_draft", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32), ("max_position", ctypes.c_int64), ("rope_theta", ctypes.c_double),
+        ("softmax_scale", ctypes.c_float), ("reserved", ctypes.c_int32), ("page_stride", ctypes.c_int64),
+        ("head_stride", ctypes.c_int64), ("slot_stride", ctypes.c_int64),
+    ]
+
+
+class KvshotError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {STATUS_NAMES.get(status, status)} ({status})")
+        self.status = status
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+
+
+def load_library(path: Optional[str] = None):
+    """Load the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2604_26412_amd.build`")
+    lib = ctypes.CDLL(p)
+    sig = {
+        "kvshot_draft_attn_init": [ctypes.POINTER(KvshotConfig), ctypes.POINTER(_vp)],
+        "kvshot_draft_attn_destroy": [_vp],
+        "kvshot_draft_attn_step": [_vp, _i32, _i32, _i32] + [_vp] * 10 + [_vp],
+        "kvshot_draft_attn_tree": [_vp, _i32, _i32, _i32] + [_vp] * 10 + [_vp],
+        "kvshot_draft_attn_validate": [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_i32), _vp],
+        "kvshot_draft_attn_set_option": [_vp, _i32, _i64],
+        "kvshot_draft_attn_plan": [_vp, _i32, _i32, _i32] + [ctypes.POINTER(_i32)] * 4,
+        "kvshot_draft_attn_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(_i64)],
+        "kvshot_debug_gather_kv": [_vp, _i32, _i32] + [_vp] * 7,
+        "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.kvshot_status_string.argtypes = [_i32]
+    lib.kvshot_status_string.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(fn: str, status: int):
+    if status != KVSHOT_OK:
+        raise KvshotError(fn, status)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(name: str) -> int:
+    if name in ("bf16", "bfloat16"):
+        return BF16
+    if name in ("fp32", "float32"):
+        return FP32
+    raise ValueError(f"dtype must be bf16 or fp32, got {name!r}")
+
+
+class DraftAttention:
+    """One configured handle of the library (see ``kvshot_config`` in the header)."""
+
+    def __init__(self, *, num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128, page_size: int = 16,
+                 dtype: str = "bf16", out_dtype: Optional[str] = None, max_batch: int, max_draft: int,
+                 max_pages_per_seq: int, num_pages: int, max_position: Optional[int] = None,
+                 rope_theta: float = 1e6, softmax_scale: float = 0.0, page_stride: int = 0, head_stride: int = 0,
+                 slot_stride: int = 0):
+        self._lib = load_library()
+        cfg = KvshotConfig()
+        cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim = num_q_heads, num_kv_heads, head_dim
+        cfg.page_size = page_size
+        cfg.dtype = _dtype_code(dtype)
+        cfg.out_dtype = _dtype_code(out_dtype or dtype)
+        cfg.max_batch, cfg.max_draft = max_batch, max_draft
+        cfg.max_pages_per_seq, cfg.num_pages = max_pages_per_seq, num_pages
+        cfg.max_position = max_position if max_position is not None else max_pages_per_seq * page_size + max_draft
+        cfg.rope_theta, cfg.softmax_scale, cfg.reserved = rope_theta, softmax_scale, 0
+        cfg.page_stride, cfg.head_stride, cfg.slot_stride = page_stride, head_stride, slot_stride
+        self.cfg = cfg
+        self.dtype = dtype
+        self.out_dtype = out_dtype or dtype
+        h = _vp()
+        _check("kvshot_draft_attn_init", self._lib.kvshot_draft_attn_init(ctypes.byref(cfg), ctypes.byref(h)))
+        self._h = h
+
+    # -- lifetime ---------------------------------------------------------
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            self._lib.kvshot_draft_attn_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    # -- argument marshalling ----------------------------------------------
+    def _elem_dtype(self):
+        torch = _torch()
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    def _tensor(self, t, name, dtype, shape=None, ndim=None):
+        torch = _torch()
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
+        if dtype is not None and t.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if shape is not None and tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if ndim is not None and t.dim() != ndim:
+            raise ValueError(f"{name} must have {ndim} dims")
+        return t.data_ptr()
+
+    def _common(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse):
+        torch = _torch()
+        c = self.cfg
+        ed = self._elem_dtype()
+        B, n = q.shape[0], q.shape[1]
+        D, Hq, Hkv = c.head_dim, c.num_q_heads, c.num_kv_heads
+        ptrs = dict(
+            q=self._tensor(q, "q", ed, (B, n, Hq, D)),
+            k=self._tensor(k_pages, "k_pages", ed),
+            v=self._tensor(v_pages, "v_pages", ed),
+            pt=self._tensor(page_table, "page_table", torch.int32, (B, c.max_pages_per_seq)),
+            lens=self._tensor(ctx_lens, "ctx_lens", torch.int32, (B,)),
+            dk=self._tensor(draft_k, "draft_k", ed, (B, c.max_draft, Hkv, D)),
+            dv=self._tensor(draft_v, "draft_v", ed, (B, c.max_draft, Hkv, D)),
+        )
+        if k_pages.numel() < c.num_pages * (c.page_stride or Hkv * c.page_size * D):
+            raise ValueError("k_pages smaller than num_pages pages")
+        if v_pages.numel() < c.num_pages * (c.page_stride or Hkv * c.page_size * D):
+            raise ValueError("v_pages smaller than num_pages pages")
+        od = torch.bfloat16 if self.out_dtype == "bf16" else torch.float32
+        if out is None:
+            out = torch.empty((B, n, Hq, D), dtype=od, device=q.device)
+        ptrs["out"] = self._tensor(out, "out", od, (B, n, Hq, D))
+        ptrs["lse"] = self._tensor(lse, "lse", torch.float32, (B, n, Hq)) if lse is not None else None
+        return ptrs, out
+
+    @staticmethod
+    def _stream(stream):
+        if stream is not None:
+            return stream
+        return _torch().cuda.current_stream().cuda_stream
+
+    def _hint(self, max_ctx):
+        return self.cfg.max_pages_per_seq * self.cfg.page_size if max_ctx is None else int(max_ctx)
+
+    # -- calls -------------------------------------------------------------
+    def step(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, step_offsets, *, max_ctx=None,
+             out=None, lse=None, stream=None):
+        """Causal draft steps; returns ``out`` [B][n_new][Hq][D]."""
+        torch = _torch()
+        ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
+        offs = self._tensor(step_offsets, "step_offsets", torch.int32, (q.shape[0],))
+        _check("kvshot_draft_attn_step", self._lib.kvshot_draft_attn_step(
+            self._h, q.shape[0], q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
+            ptrs["lens"], ptrs["dk"], ptrs["dv"], offs, ptrs["out"], ptrs["lse"], self._stream(stream)))
+        return out
+
+    def tree(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, parents, *, max_ctx=None,
+             out=None, lse=None, stream=None):
+        """Draft-tree nodes with an ancestor-or-self mask; returns ``out`` [B][n_nodes][Hq][D]."""
+        torch = _torch()
+        ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
+        par = self._tensor(parents, "parents", torch.int32, (q.shape[0], q.shape[1]))
+        _check("kvshot_draft_attn_tree", self._lib.kvshot_draft_attn_tree(
+            self._h, q.shape[0], q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
+            ptrs["lens"], ptrs["dk"], ptrs["dv"], par, ptrs["out"], ptrs["lse"], self._stream(stream)))
+        return out
+
+    def validate(self, page_table, ctx_lens, n_queries, *, step_offsets=None, parents=None, max_ctx=None,
+                 stream=None):
+        """Returns 0 if the device data honours the contract, else the first violation code (1..4)."""
+        torch = _torch()
+        B = ctx_lens.shape[0]
+        pt = self._tensor(page_table, "page_table", torch.int32, (B, self.cfg.max_pages_per_seq))
+        lens = self._tensor(ctx_lens, "ctx_lens", torch.int32, (B,))
+        so = self._tensor(step_offsets, "step_offsets", torch.int32, (B,)) if step_offsets is not None else None
+        par = self._tensor(parents, "parents", torch.int32, (B, n_queries)) if parents is not None else None
+        bad = _i32(0)
+        st = self._lib.kvshot_draft_attn_validate(self._h, B, n_queries, self._hint(max_ctx), pt, lens, so, par,
+                                                  ctypes.byref(bad), self._stream(stream))
+        if st not in (KVSHOT_OK, 5):
+            raise KvshotError("kvshot_draft_attn_validate", st)
+        return int(bad.value)
+
+    def set_option(self, option: int, value: int):
+        _check("kvshot_draft_attn_set_option", self._lib.kvshot_draft_attn_set_option(self._h, option, value))
+
+    def plan(self, batch: int, n_queries: int, max_ctx: Optional[int] = None):
+        vals = [_i32(0) for _ in range(4)]
+        _check("kvshot_draft_attn_plan", self._lib.kvshot_draft_attn_plan(
+            self._h, batch, n_queries, self._hint(max_ctx), *[ctypes.byref(v) for v in vals]))
+        return dict(splits=vals[0].value, path=vals[1].value, row_tiles=vals[2].value, workgroups=vals[3].value)
+
+    def profile_read(self):
+        a, c, n = ctypes.c_double(0), ctypes.c_double(0), _i64(0)
+        _check("kvshot_draft_attn_profile_read", self._lib.kvshot_draft_attn_profile_read(
+            self._h, ctypes.byref(a), ctypes.byref(c), ctypes.byref(n)))
+        return dict(attn_ms=a.value, combine_ms=c.value, calls=n.value)
+
+    def debug_gather_kv(self, k_pages, v_pages, page_table, ctx_lens, max_ctx, stream=None):
+        torch = _torch()
+        c = self.cfg
+        ed = self._elem_dtype()
+        B = ctx_lens.shape[0]
+        kd = torch.empty((B, max_ctx, c.num_kv_heads, c.head_dim), dtype=ed, device=k_pages.device)
+        vd = torch.empty_like(kd)
+        _check("kvshot_debug_gather_kv", self._lib.kvshot_debug_gather_kv(
+            self._h, B, max_ctx, self._tensor(k_pages, "k_pages", ed), self._tensor(v_pages, "v_pages", ed),
+            self._tensor(page_table, "page_table", torch.int32, (B, c.max_pages_per_seq)),
+            self._tensor(ctx_lens, "ctx_lens", torch.int32, (B,)), kd.data_ptr(), vd.data_ptr(),
+            self._stream(stream)))
+        return kd, vd
+
+    def debug_tree_mask(self, parents, stream=None):
+        torch = _torch()
+        B, n = parents.shape
+        anc = torch.empty((B, n), dtype=torch.int64, device=parents.device)
+        depth = torch.empty((B, n), dtype=torch.int32, device=parents.device)
+        _check("kvshot_debug_tree_mask", self._lib.kvshot_debug_tree_mask(
+            self._h, B, n, self._tensor(parents, "parents", torch.int32, (B, n)), anc.data_ptr(), depth.data_ptr(),
+            self._stream(stream)))
+        return anc, depth

@@ -1,0 +1,88 @@
+// Debug and validation kernels.  They run the same index code as the
+// attention kernels (kvshot_common.h) so tests can check that code bit for bit.
+#include "kvshot_common.h"
+
+namespace kvshot {
+namespace {
+
+// One thread per (token, 16-byte chunk) of the dense logical view.
+__global__ __launch_bounds__(256) void gather_kv_kernel(AttnParams p, int max_ctx, void* k_dense, void* v_dense,
+                                                        int elem_bytes) {
+  const int chunks = kHeadDim * elem_bytes / 16;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int tok = (int)(idx / chunks), ch = (int)(idx % chunks);
+  if (tok >= max_ctx) return;
+  const int T = clamp_ctx(p.ctx_lens[b], p.max_pages_per_seq, p.page_shift);
+  const int64_t dst = ((((int64_t)b * max_ctx + tok) * p.hkv + h) * kHeadDim) * elem_bytes + ch * 16;
+  uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+  if (tok < T) {
+    const int pid = physical_page(p.page_table, b, p.max_pages_per_seq, tok >> p.page_shift, p.num_pages);
+    const int64_t off = kv_offset(pid, h, tok & ((1 << p.page_shift) - 1), p.page_stride, p.head_stride,
+                                  p.slot_stride) * elem_bytes + ch * 16;
+    kv = *(const uint4*)((const unsigned char*)p.k_pages + off);
+    vv = *(const uint4*)((const unsigned char*)p.v_pages + off);
+  }
+  *(uint4*)((unsigned char*)k_dense + dst) = kv;
+  *(uint4*)((unsigned char*)v_dense + dst) = vv;
+}
+
+// One wave per sequence.
+__global__ __launch_bounds__(64) void tree_mask_kernel(const int32_t* parents, int n, uint64_t* anc, int32_t* depth) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  int d = 0;
+  const uint64_t a = tree_ancestry_wave(parents + (int64_t)b * n, n, lane, &d);
+  if (lane < n) {
+    anc[(int64_t)b * n + lane] = a;
+    depth[(int64_t)b * n + lane] = d;
+  }
+}
+
+__global__ void flag_init_kernel(int32_t* flag) { *flag = 0x7fffffff; }
+
+// One workgroup per sequence: checks its length, its used page ids, its step
+// offset and its parents; records the smallest violation code seen.
+__global__ __launch_bounds__(256) void validate_kernel(AttnParams p, int max_ctx_hint, int32_t* flag) {
+  const int b = blockIdx.x;
+  const int t = threadIdx.x;
+  const int T = p.ctx_lens[b];
+  if (t == 0 && (T < 0 || T > max_ctx_hint)) atomicMin(flag, 1);
+  const int Tc = T < 0 ? 0 : (T > max_ctx_hint ? max_ctx_hint : T);
+  const int used = (Tc + (1 << p.page_shift) - 1) >> p.page_shift;
+  for (int lp = t; lp < used; lp += 256) {
+    const int pid = p.page_table[(int64_t)b * p.max_pages_per_seq + lp];
+    if (pid < 0 || pid >= p.num_pages) atomicMin(flag, 2);
+  }
+  if (p.step_offsets && t == 0) {
+    const int s0 = p.step_offsets[b];
+    if (s0 < 0 || s0 + p.nq > p.max_draft) atomicMin(flag, 3);
+  }
+  if (p.parents && t < p.nq) {
+    const int par = p.parents[(int64_t)b * p.nq + t];
+    if (par < -1 || par >= t) atomicMin(flag, 4);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather_kv(const AttnParams& p, int max_ctx, void* k_dense, void* v_dense, int bf16,
+                            hipStream_t s) {
+  const int eb = bf16 ? 2 : 4;
+  const int64_t threads = (int64_t)max_ctx * (kHeadDim * eb / 16);
+  const dim3 grid((unsigned)((threads + 255) / 256), p.hkv, p.batch);
+  hipLaunchKernelGGL(gather_kv_kernel, grid, dim3(256), 0, s, p, max_ctx, k_dense, v_dense, eb);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_mask(const int32_t* parents, int batch, int n, uint64_t* anc, int32_t* depth, hipStream_t s) {
+  hipLaunchKernelGGL(tree_mask_kernel, dim3(batch), dim3(64), 0, s, parents, n, anc, depth);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const AttnParams& p, int max_ctx_hint, int32_t* flag, hipStream_t s) {
+  hipLaunchKernelGGL(flag_init_kernel, dim3(1), dim3(1), 0, s, flag);
+  hipLaunchKernelGGL(validate_kernel, dim3(p.batch), dim3(256), 0, s, p, max_ctx_hint, flag);
+  return hipGetLastError();
+}
+
+}  // namespace kvshot

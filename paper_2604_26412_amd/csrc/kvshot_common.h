@@ -1,0 +1,138 @@
+// Internal definitions shared by the draft-attention kernels and the host API.
+//
+// Device-side index code lives here once: logical token -> (page, slot) ->
+// element offset, draft position, and the tree ancestry of a wave's nodes.
+// The attention kernels and the debug exports both call these functions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvshot {
+
+constexpr int kHeadDim = 128;
+constexpr int kHalfDim = 64;          // RoPE pairs (m, m + 64)
+constexpr int kBlockKeys = 32;        // keys per inner-loop block (one 32x32 MFMA tile)
+constexpr int kMaxDraft = 64;         // tree masks are 64-bit
+constexpr int kMaxSplits = 64;
+constexpr int kMaxRows = 256;         // G * queries per (sequence, KV head)
+
+// Everything one attention launch needs; passed by value.
+struct AttnParams {
+  const void* q;                // [B][nq][Hq][D]
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* page_table;    // [B][max_pages_per_seq]
+  const int32_t* ctx_lens;      // [B]
+  const void* draft_k;          // [B][max_draft][Hkv][D]
+  const void* draft_v;
+  const int32_t* step_offsets;  // [B] (step mode) or null
+  const int32_t* parents;       // [B][nq] (tree mode) or null
+  const float2* rope;           // [max_position][64] (cos, sin)
+  void* out;                    // [B][nq][Hq][D]
+  float* lse;                   // [B][nq][Hq] or null
+  float* part_o;                // [B][Hkv][rows_pad][splits][D]
+  float2* part_ml;              // [B][Hkv][rows_pad][splits] (max in log2 units, sum)
+  int64_t page_stride, head_stride, slot_stride;  // elements
+  int32_t batch, nq, hq, hkv, group;
+  int32_t page_shift, max_pages_per_seq, num_pages, max_draft;
+  int32_t rows, rows_pad;       // rows = group * nq
+  int32_t splits, blocks_per_split, max_ctx;
+  int32_t max_position;
+  int32_t tree;                 // 0 step, 1 tree
+  int32_t out_fp32;
+  float qscale;                 // softmax scale * log2(e): scores come out in log2 units
+};
+
+struct CombineParams {
+  const float* part_o;
+  const float2* part_ml;
+  void* out;
+  float* lse;
+  int32_t batch, nq, hq, hkv, group, rows, rows_pad, splits, out_fp32;
+};
+
+// ---------------------------------------------------------------------------
+// bf16 helpers (bit patterns in uint16)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Round-to-nearest-even float -> bf16 bits (compiles to v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  bf16x2_t v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// ---------------------------------------------------------------------------
+// index code
+// ---------------------------------------------------------------------------
+
+// Prefix length actually served: clamped to what the page table row can hold.
+__device__ __forceinline__ int clamp_ctx(int t, int max_pages_per_seq, int page_shift) {
+  const int cap = max_pages_per_seq << page_shift;
+  return t < 0 ? 0 : (t > cap ? cap : t);
+}
+
+// Physical page holding logical page `lpage` of sequence b (clamped into the pool).
+__device__ __forceinline__ int physical_page(const int32_t* page_table, int b, int max_pages_per_seq,
+                                             int lpage, int num_pages) {
+  int pid = page_table[(int64_t)b * max_pages_per_seq + lpage];
+  pid = pid < 0 ? 0 : pid;
+  return pid >= num_pages ? num_pages - 1 : pid;
+}
+
+// Element offset of (page, kv_head, slot, d = 0).
+__device__ __forceinline__ int64_t kv_offset(int pid, int head, int slot, int64_t page_stride,
+                                             int64_t head_stride, int64_t slot_stride) {
+  return (int64_t)pid * page_stride + (int64_t)head * head_stride + (int64_t)slot * slot_stride;
+}
+
+// Element offset of draft row s of sequence b, KV head h.
+__device__ __forceinline__ int64_t draft_offset(int b, int s, int h, int max_draft, int hkv) {
+  return (((int64_t)b * max_draft + s) * hkv + h) * kHeadDim;
+}
+
+// Tree ancestry of the (up to 64) nodes of one sequence, one node per lane.
+// Returns the ancestor-or-self bitmask of node `lane` and sets its depth.
+// Pointer jumping: after k rounds each lane holds the ancestors within
+// distance < 2^k and a pointer to the one at distance 2^k; six rounds cover
+// any chain of 64 nodes.  A parent outside {-1} U [0, i) is treated as a root.
+__device__ __forceinline__ uint64_t tree_ancestry_wave(const int32_t* parents_row, int n, int lane, int* depth) {
+  int p = -1;
+  if (lane < n) {
+    p = parents_row[lane];
+    if (p < -1 || p >= lane) p = -1;
+  }
+  uint64_t anc = lane < n ? (1ull << lane) : 0ull;
+  int jump = p;
+#pragma unroll
+  for (int it = 0; it < 6; ++it) {
+    const int src = jump >= 0 ? jump : lane;
+    const uint32_t lo = __shfl((uint32_t)anc, src);
+    const uint32_t hi = __shfl((uint32_t)(anc >> 32), src);
+    const int jj = __shfl(jump, src);
+    if (jump >= 0) {
+      anc |= ((uint64_t)hi << 32) | lo;
+      jump = jj;
+    }
+  }
+  *depth = lane < n ? __popcll(anc) - 1 : 0;
+  return anc;
+}
+
+}  // namespace kvshot
+
+// Launchers (defined in the .hip files).
+namespace kvshot {
+hipError_t launch_attn_mfma(const AttnParams& p, int row_tiles, hipStream_t s);
+hipError_t launch_attn_generic(const AttnParams& p, int bf16_in, hipStream_t s);
+hipError_t launch_combine(const CombineParams& p, hipStream_t s);
+hipError_t launch_gather_kv(const AttnParams& p, int max_ctx, void* k_dense, void* v_dense, int bf16, hipStream_t s);
+hipError_t launch_tree_mask(const int32_t* parents, int batch, int n, uint64_t* anc, int32_t* depth, hipStream_t s);
+hipError_t launch_validate(const AttnParams& p, int max_ctx_hint, int32_t* flag, hipStream_t s);
+int mfma_waves_per_wg(int row_tiles);
+}  // namespace kvshot

@@ -1,0 +1,124 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared
+function, and rejects bad arguments on the host before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2604_26412_amd as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(K.LIB_PATH):
+        from paper_2604_26412_amd import build
+        build.build()
+    return K.load_library()
+
+
+def declared_functions():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z_0-9]*\s*\*?\s*(kvshot_[a-z_0-9]+)\s*\(", text,
+                                flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_binding_symbols():
+    assert declared_functions() == sorted(K.EXPORTED_SYMBOLS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def good_cfg(**kw):
+    c = K.KvshotConfig()
+    c.num_q_heads, c.num_kv_heads, c.head_dim, c.page_size = 32, 8, 128, 16
+    c.dtype, c.out_dtype, c.max_batch, c.max_draft = 0, 0, 4, 8
+    c.max_pages_per_seq, c.num_pages, c.max_position = 16, 64, 300
+    c.rope_theta, c.softmax_scale, c.reserved = 1e6, 0.0, 0
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=64), 2),
+    (dict(num_q_heads=30), 1),
+    (dict(num_q_heads=128, num_kv_heads=8), 2),
+    (dict(page_size=24), 1),
+    (dict(page_size=8), 1),
+    (dict(page_size=512), 1),
+    (dict(max_draft=65), 1),
+    (dict(max_draft=0), 1),
+    (dict(dtype=7), 1),
+    (dict(out_dtype=-1), 1),
+    (dict(max_batch=0), 1),
+    (dict(num_pages=0), 1),
+    (dict(max_position=0), 1),
+    (dict(rope_theta=0.0), 1),
+    (dict(rope_theta=float("nan")), 1),
+    (dict(softmax_scale=-1.0), 1),
+    (dict(reserved=3), 1),
+    (dict(slot_stride=100), 1),
+])
+def test_init_rejects_bad_configs_before_any_device_call(lib, kw, status):
+    h = ctypes.c_void_p(123)
+    assert lib.kvshot_draft_attn_init(ctypes.byref(good_cfg(**kw)), ctypes.byref(h)) == status
+    assert h.value is None
+
+
+def test_null_arguments(lib):
+    h = ctypes.c_void_p()
+    assert lib.kvshot_draft_attn_init(None, ctypes.byref(h)) == 1
+    assert lib.kvshot_draft_attn_init(ctypes.byref(good_cfg()), None) == 1
+    assert lib.kvshot_draft_attn_step(None, 1, 1, 16, *([None] * 10), None) == 1
+    assert lib.kvshot_draft_attn_tree(None, 1, 1, 16, *([None] * 10), None) == 1
+    assert lib.kvshot_draft_attn_set_option(None, 0, 0) == 1
+    assert lib.kvshot_draft_attn_plan(None, 1, 1, 16, None, None, None, None) == 1
+    assert lib.kvshot_draft_attn_profile_read(None, None, None, None) == 1
+    assert lib.kvshot_debug_tree_mask(None, 1, 1, None, None, None, None) == 1
+    assert lib.kvshot_debug_gather_kv(None, 1, 1, *([None] * 7)) == 1
+    assert lib.kvshot_draft_attn_validate(None, 1, 1, 16, None, None, None, None, None, None) == 1
+    assert lib.kvshot_draft_attn_destroy(None) == 0
+
+
+def test_status_strings(lib):
+    assert lib.kvshot_status_string(0) == b"ok"
+    assert lib.kvshot_status_string(5).startswith(b"contract")
+    assert lib.kvshot_status_string(99) == b"unknown status"
+
+
+def test_config_struct_layout_matches_header():
+    # int32 x10, int64, double, float, int32, int64 x3
+    assert ctypes.sizeof(K.KvshotConfig) == 10 * 4 + 8 + 8 + 4 + 4 + 3 * 8
+    assert K.KvshotConfig.max_position.offset == 40
+    assert K.KvshotConfig.page_stride.offset == 64
+
+
+def test_product_path_does_not_import_the_oracle():
+    src = open(os.path.join(ROOT, "paper_2604_26412_amd", "__init__.py")).read()
+    assert "oracle" not in src.replace("no fallback", "")
+    for fn in os.listdir(os.path.join(ROOT, "paper_2604_26412_amd", "csrc")):
+        assert "oracle" not in open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", fn)).read().lower()
+
+
+def test_binding_argument_counts_match_header(lib):
+    text = ""
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text += open(os.path.join(ROOT, "include", fn)).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    for name in declared_functions():
+        m = re.search(name + r"\s*\(([^;]*?)\)\s*;", text, flags=re.S)
+        assert m, name
+        params = [p for p in m.group(1).split(",") if p.strip() and p.strip() != "void"]
+        assert len(getattr(lib, name).argtypes) == len(params), name
