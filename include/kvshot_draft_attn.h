@@ -165,6 +165,12 @@ kvshot_status kvshot_debug_gather_kv(kvshot_handle h, int32_t batch, int32_t max
 kvshot_status kvshot_debug_tree_mask(kvshot_handle h, int32_t batch, int32_t n_nodes, const int32_t* parents,
                                      uint64_t* anc_out, int32_t* depth_out, void* stream);
 
+/* Measurement helper: reads `bytes` (rounded down to a multiple of 16) of
+ * device memory `src` once with 16-byte loads, using `sink_words` workgroups;
+ * each workgroup writes one 16-byte word of `sink` (device, >= 16*sink_words
+ * bytes).  Times the device's practical streaming-read bandwidth. */
+kvshot_status kvshot_debug_stream_read(const void* src, int64_t bytes, void* sink, int32_t sink_words, void* stream);
+
 /* Static text for a status code. */
 const char* kvshot_status_string(int32_t status);
 

@@ -26,7 +26,8 @@ OPT_SPLITS, OPT_PATH, OPT_PROFILE = 0, 1, 2
 EXPORTED_SYMBOLS = [
     "kvshot_draft_attn_init", "kvshot_draft_attn_destroy", "kvshot_draft_attn_step", "kvshot_draft_attn_tree",
     "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
-    "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_status_string",
+    "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_debug_stream_read",
+    "kvshot_status_string",
 ]
 
 
@@ -74,6 +75,7 @@ def load_library(path: Optional[str] = None):
                                            ctypes.POINTER(_i64)],
         "kvshot_debug_gather_kv": [_vp, _i32, _i32] + [_vp] * 7,
         "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
+        "kvshot_debug_stream_read": [_vp, _i64, _vp, _i32, _vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -102,6 +104,18 @@ def _dtype_code(name: str) -> int:
     if name in ("fp32", "float32"):
         return FP32
     raise ValueError(f"dtype must be bf16 or fp32, got {name!r}")
+
+
+def stream_read(src, sink=None, workgroups: int = 2048, stream=None):
+    """Read every byte of device tensor `src` once (streaming-read bandwidth probe)."""
+    torch = _torch()
+    lib = load_library()
+    if sink is None:
+        sink = torch.empty(workgroups * 4, dtype=torch.int32, device=src.device)
+    st = lib.kvshot_debug_stream_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(), workgroups,
+                                      stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+    _check("kvshot_debug_stream_read", st)
+    return sink
 
 
 class DraftAttention:

@@ -88,10 +88,12 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
   if (c->opt_splits > 0) {
     splits = c->opt_splits;
   } else {
-    // enough workgroups for several rounds over the chip, but keep >= 8 blocks per wave
-    const int target_wgs = c->num_cus * 8;
+    // One round of workgroups over the chip (two 4-wave or one 8-wave workgroup
+    // per CU are resident at once); split the context only when the (sequence,
+    // KV head) pairs alone leave CUs idle, and keep >= 4 blocks per wave.
+    const int target_wgs = c->num_cus * (8 / pl.waves_per_wg);
     splits = (target_wgs + pairs - 1) / pairs;
-    const int cap = nb / (pl.key_streams * 8);
+    const int cap = nb / (pl.key_streams * 4);
     splits = splits > cap ? cap : splits;
   }
   if (splits < 1) splits = 1;
@@ -479,6 +481,14 @@ kvshot_status kvshot_debug_tree_mask(kvshot_handle h, int32_t batch, int32_t n_n
   if (st != KVSHOT_OK) return st;
   if (launch_tree_mask(parents, batch, n_nodes, anc_out, depth_out, (hipStream_t)stream) != hipSuccess)
     return KVSHOT_ERR_DEVICE;
+  return KVSHOT_OK;
+}
+
+kvshot_status kvshot_debug_stream_read(const void* src, int64_t bytes, void* sink, int32_t sink_words,
+                                       void* stream) {
+  if (!src || !sink || bytes < 16 || sink_words < 1 || !aligned16(src) || !aligned16(sink))
+    return KVSHOT_ERR_INVALID_ARG;
+  if (launch_stream_read(src, bytes, sink, sink_words, (hipStream_t)stream) != hipSuccess) return KVSHOT_ERR_DEVICE;
   return KVSHOT_OK;
 }
 

@@ -6,16 +6,25 @@
 // them (grouped-query folding).  The memory attended is the target prefix of
 // the sequence followed by its draft keys (Sec. 3.4.1, Eq. 7; App. B).
 //
-// Per 32-key block a wave computes S^T = K * Q^T with v_mfma_f32_32x32x16_bf16,
-// so each lane ends up owning one query row (lane % 32) and 16 of the block's
-// keys: the online-softmax row max needs one cross-half exchange and the
-// rescale of the output accumulator is lane-local.  O^T = V^T * P^T runs on the
-// same MFMA; V is transposed through LDS.  K goes straight from HBM into the
-// MFMA operand registers.
+// Data movement per 32-key block: K and V rows are read from HBM with fully
+// coalesced 16-byte non-temporal loads (each load instruction covers four
+// whole 256-byte rows) into registers, then written row-major into LDS.
+// MFMA operands come back out of LDS: K rows with ds_read_b128, and V
+// transposed with ds_read_b64_tr_b16 (each 16-lane group turns a 4-key x
+// 16-channel tile into 4 keys per channel lane).
+//
+// Math per block and wave: S^T = K * Q^T (v_mfma_f32_32x32x16_bf16), so each
+// lane owns one query row (lane % 32) and 16 of the block's keys; the online
+// softmax row max needs one cross-half exchange and the output rescale is
+// lane-local.  O^T += V^T * P^T on the same MFMA, with P taken straight from
+// the S^T accumulator (the K rows are permuted so that the accumulator layout
+// is the B-operand layout of the second product).
 //
 // Row tiles: rows are padded to 32 * RT.  A workgroup has NW waves; wave w
-// owns row tile w % RT and key stream w / RT; the KS = NW / RT key streams
-// interleave 32-key blocks and are merged through LDS at the end.
+// owns row tile w % RT and key stream w / RT.  The RT waves of a key stream
+// share its LDS tiles (each loads 8 / RT of the block's load instructions);
+// the KS = NW / RT key streams interleave blocks and merge through LDS at the
+// end.
 #include "kvshot_common.h"
 
 namespace kvshot {
@@ -26,9 +35,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kVtPitch = 40;                               // bf16 per V^T row: 32 keys + 8 pad (80 B)
-constexpr int kVtBytes = kHeadDim * kVtPitch * 2;          // 10 KB per wave
+// LDS row pitches (bf16 elements).  K rows are read 16 rows x 16 bytes at a
+// time (pitch = 68 dwords spreads them over distinct banks); V rows are read by
+// the transpose load 4 rows x 32 bytes per 16 lanes (pitch = 80 dwords).
+constexpr int kKPitch = 136;
+constexpr int kVPitch = 160;
+constexpr int kKTileBytes = kBlockKeys * kKPitch * 2;    // 8704
+constexpr int kVTileBytes = kBlockKeys * kVPitch * 2;    // 10240
+constexpr int kStreamBytes = kKTileBytes + kVTileBytes;
 constexpr float kLn2 = 0.693147180559945309f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -40,8 +56,8 @@ __device__ __forceinline__ int32_t load_scalar_i32(const int32_t* base, int64_t 
   return cp[idx];
 }
 
-// Rotate one lane's (d, d + 64) pairs by the table angles and scale; q chunk kc
-// holds d = kc * 16 + hh * 8 + e, so chunks kc and kc + 4 pair up in-lane.
+// Rotate one lane's (d, d + 64) pairs by the table angles and scale.  Operand
+// chunk kc holds d = kc * 16 + hh * 8 + e, so chunks kc and kc + 4 pair up in-lane.
 __device__ __forceinline__ void rope_rotate_to_bf16(const u32x4 (&raw)[8], const float2* cs, float scale,
                                                     bf16x8 (&dst)[8]) {
 #pragma unroll
@@ -63,33 +79,15 @@ __device__ __forceinline__ void rope_rotate_to_bf16(const u32x4 (&raw)[8], const
   }
 }
 
-// Write one lane's V chunk (key `key`, d = t * 16 + hh * 8 + e) transposed into V^T.
-__device__ __forceinline__ void store_vt(uint16_t* vt, const u32x4 (&v)[8], int key, int hh) {
-#pragma unroll
-  for (int t = 0; t < 8; ++t) {
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      const int d = t * 16 + hh * 8 + 2 * e2;
-      vt[d * kVtPitch + key] = (uint16_t)(v[t][e2] & 0xffffu);
-      vt[(d + 1) * kVtPitch + key] = (uint16_t)(v[t][e2] >> 16);
-    }
-  }
-}
-
 struct SoftmaxState {
   float m;   // running max (log2 units), identical in both lane halves
   float l;   // this lane's partial sum over its keys
 };
 
-// One 32-key block: S^T from K operands, masked online softmax, O^T += V^T P^T.
+// Softmax update and O^T += V^T P^T for one block whose scores are in `s`.
 // `valid` bit v: key of accumulator register v is visible to this lane's row.
-__device__ __forceinline__ void attend_block(const bf16x8 (&kop)[8], const bf16x8 (&qop)[8], const uint16_t* vt,
-                                             int l32, int hh, uint32_t valid, f32x16 (&oacc)[4],
-                                             SoftmaxState& st) {
-  f32x16 s = {};
-#pragma unroll
-  for (int kc = 0; kc < 8; ++kc) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qop[kc], s, 0, 0, 0);
-
+__device__ __forceinline__ void softmax_pv(f32x16 s, const uint16_t* vtile, int vt_off, uint32_t valid,
+                                           f32x16 (&oacc)[4], SoftmaxState& st) {
   float bm = -INFINITY;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -117,27 +115,47 @@ __device__ __forceinline__ void attend_block(const bf16x8 (&kop)[8], const bf16x
 #pragma unroll
       for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
   }
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const __attribute__((address_space(3))) uint16_t* vb =
+      (const __attribute__((address_space(3))) uint16_t*)(vtile) + vt_off;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
-      const u32x4 a = *(const u32x4*)(vt + (dt * 32 + l32) * kVtPitch + 16 * sidx + 8 * hh);
+      // keys 16*sidx + 8*hh + 0..3 and + 4..7 of channel dt*32 + lane%32
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4*)(vb + (16 * sidx) * kVPitch + dt * 32));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4*)(vb + (16 * sidx + 4) * kVPitch + dt * 32));
+      const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
       oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pw[sidx]), oacc[dt], 0, 0, 0);
     }
   }
 }
 
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+template <int RT>
+__device__ __forceinline__ void tile_sync() {
+  if constexpr (RT > 1) {
+    __syncthreads();
+  } else {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
 }
 
+#ifndef KVSHOT_MFMA_WAVES_PER_SIMD
+#define KVSHOT_MFMA_WAVES_PER_SIMD 2
+#endif
+
 template <int RT, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnParams p) {
+__global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma_kernel(AttnParams p) {
   constexpr int KS = NW / RT;
+  constexpr int kLoadsPerWave = 8 / RT;   // 16-byte load instructions per K (and per V) tile and wave
   constexpr int kMergeBytes = (KS - 1) * RT * 64 * (64 * 4 + 8);
-  constexpr int kLdsBytes = (NW * kVtBytes > kMergeBytes) ? NW * kVtBytes : kMergeBytes;
+  constexpr int kTileBytes = KS * kStreamBytes;
+  constexpr int kLdsBytes = kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
 
   const int lane = threadIdx.x & 63;
@@ -153,6 +171,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnParams p) {
   const int nbt = (T + kBlockKeys - 1) / kBlockKeys;
   const int blk0 = split * p.blocks_per_split;
   const int blk1 = min(blk0 + p.blocks_per_split, nbt);
+  const int nt = blk1 > blk0 ? blk1 - blk0 : 0;
   const bool last = split == p.splits - 1;
 
   int s0 = 0, S = p.nq;
@@ -161,6 +180,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnParams p) {
     s0 = s0 < 0 ? 0 : (s0 > p.max_draft - p.nq ? p.max_draft - p.nq : s0);
     S = s0 + p.nq;
   }
+  const int nd = last ? (S + kBlockKeys - 1) / kBlockKeys : 0;
 
   // query row of this lane
   const int r = rt * 32 + l32;
@@ -192,130 +212,143 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnParams p) {
     rope_rotate_to_bf16(raw, p.rope + (int64_t)qpos * kHalfDim + hh * 8, row_ok ? p.qscale : 0.0f, qop);
   }
 
-  uint16_t* vt = (uint16_t*)(lds + w * kVtBytes);
+  uint16_t* ktile = (uint16_t*)(lds + ks * kStreamBytes);
+  uint16_t* vtile = (uint16_t*)(lds + ks * kStreamBytes + kKTileBytes);
 
-  // K-operand row rho = l32 holds key kperm(rho), chosen so that accumulator
-  // register v of lane (row, hh) holds key 16 * (v / 8) + 8 * hh + v % 8.
+  // K-operand row rho = l32 reads tile row kperm(rho), chosen so that
+  // accumulator register v of lane (row, hh) holds key 16 * (v / 8) + 8 * hh + v % 8.
   const int kperm = ((l32 >> 4) << 4) + (((l32 >> 2) & 1) << 3) + (((l32 >> 3) & 1) << 2) + (l32 & 3);
+  const int k_rd = kperm * kKPitch + hh * 8;
+  // transpose-read base: 16-lane group gr reads keys 8*(gr/2) + (lane%16)/4 of
+  // channels 16*(gr%2) + 4*(lane%4) .. +3; lane i of the group receives channel
+  // 16*(gr%2) + i of four consecutive keys
+  const int gr = lane >> 4, sg = lane & 15;
+  const int vt_off = ((gr >> 1) * 8 + (sg >> 2)) * kVPitch + (gr & 1) * 16 + 4 * (sg & 3);
+  // coalesced load / LDS write slot of this lane in load instruction t: row 4t + lane/16, 16-byte chunk lane%16
+  const int ld_row = lane >> 4, ld_chunk = lane & 15;
 
   f32x16 oacc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) oacc[dt] = f32x16{};
   SoftmaxState st{-INFINITY, 0.0f};
 
-  const int64_t ps = p.page_stride, hs = p.head_stride, ss = p.slot_stride;
+  const int64_t pstr = p.page_stride, hstr = p.head_stride, sstr = p.slot_stride;
   const uint16_t* kbase = (const uint16_t*)p.k_pages;
   const uint16_t* vbase = (const uint16_t*)p.v_pages;
+  const uint16_t* dkbase = (const uint16_t*)p.draft_k;
+  const uint16_t* dvbase = (const uint16_t*)p.draft_v;
   const int pmask = (1 << p.page_shift) - 1;
   const int lp_last = T > 0 ? (T - 1) >> p.page_shift : 0;
+  const int64_t pt_row = (int64_t)b * p.max_pages_per_seq;
 
-  // ---- target blocks: blk = blk0 + ks + KS * i ----
-  int blk = blk0 + ks;
-  u32x4 kcur[8], vcur[8];
-  int pidA = 0, pidB = 0;
-  auto block_pids = [&](int bk, int& a, int& bb) {
-    const int key0 = bk * kBlockKeys;
+  // Issue this wave's share of the loads of target block tb into kd / vd.
+  auto issue_target = [&](int tb, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
+    const int key0 = (blk0 + tb) * kBlockKeys;
     int la = key0 >> p.page_shift, lb = (key0 + 16) >> p.page_shift;
     la = la > lp_last ? lp_last : la;
     lb = lb > lp_last ? lp_last : lb;
-    const int64_t row = (int64_t)b * p.max_pages_per_seq;
-    a = load_scalar_i32(p.page_table, row + la);
-    bb = load_scalar_i32(p.page_table, row + lb);
-    a = a < 0 ? 0 : (a >= p.num_pages ? p.num_pages - 1 : a);
-    bb = bb < 0 ? 0 : (bb >= p.num_pages ? p.num_pages - 1 : bb);
+    int pa = load_scalar_i32(p.page_table, pt_row + la);
+    int pb = load_scalar_i32(p.page_table, pt_row + lb);
+    pa = pa < 0 ? 0 : (pa >= p.num_pages ? p.num_pages - 1 : pa);
+    pb = pb < 0 ? 0 : (pb >= p.num_pages ? p.num_pages - 1 : pb);
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int t = rt + RT * i;                  // load instruction index within the block
+      const int kr = 4 * t + ld_row;             // key within the block
+      const int pid = kr >= 16 ? pb : pa;        // page sizes >= 32 have pa == pb
+      const int64_t off = kv_offset(pid, h, (key0 + kr) & pmask, pstr, hstr, sstr) + ld_chunk * 8;
+      // the prefix K/V is read exactly once: whole lines, non-temporal
+      kd[i] = __builtin_nontemporal_load((const u32x4*)(kbase + off));
+      vd[i] = __builtin_nontemporal_load((const u32x4*)(vbase + off));
+    }
   };
-  auto issue_loads = [&](int bk, int a, int bb, u32x4 (&kd)[8], u32x4 (&vd)[8]) {
-    const int key0 = bk * kBlockKeys;
-    // for page sizes >= 32 both halves of the block share one page (a == bb)
-    const int kk = key0 + kperm;
-    const int kpid = (kperm >= 16) ? bb : a;
-    const uint16_t* kp = kbase + kv_offset(kpid, h, kk & pmask, ps, hs, ss) + hh * 8;
-    const int vk = key0 + l32;
-    const int vpid = (l32 >= 16) ? bb : a;
-    const uint16_t* vp = vbase + kv_offset(vpid, h, vk & pmask, ps, hs, ss) + hh * 8;
+  // Stage this wave's share of a block into the LDS tiles; rows at or past
+  // `kend` get zero V so masked weights never meet NaN.
+  auto stage = [&](int key0, int kend, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
 #pragma unroll
-    for (int kc = 0; kc < 8; ++kc) kd[kc] = *(const u32x4*)(kp + kc * 16);
-#pragma unroll
-    for (int t = 0; t < 8; ++t) vd[t] = *(const u32x4*)(vp + t * 16);
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int kr = 4 * (rt + RT * i) + ld_row;
+      if (key0 + kr >= kend) vd[i] = u32x4{0u, 0u, 0u, 0u};
+      *(u32x4*)(ktile + kr * kKPitch + ld_chunk * 8) = kd[i];
+      *(u32x4*)(vtile + kr * kVPitch + ld_chunk * 8) = vd[i];
+    }
   };
 
-  if (blk < blk1) {
-    block_pids(blk, pidA, pidB);
-    issue_loads(blk, pidA, pidB, kcur, vcur);
-  }
-  for (; blk < blk1; blk += KS) {
-    const int key0 = blk * kBlockKeys;
-    const int nblk = blk + KS;
-    int nA = 0, nB = 0;
-    if (nblk < blk1) block_pids(nblk, nA, nB);
-    const bool tail = key0 + kBlockKeys > T;
-    if (tail) {
-      // zero V rows past the prefix so masked weights never meet NaN
-      if (key0 + l32 >= T) {
+  // ---- target blocks: tb = ks + KS * it, software-pipelined one block ahead ----
+  {
+    const int iters = (nt + KS - 1) / KS;          // same for every wave of the workgroup
+    u32x4 kst[kLoadsPerWave], vst[kLoadsPerWave];
+    if (ks < nt) issue_target(ks, kst, vst);
+    for (int it = 0; it < iters; ++it) {
+      const int tb = ks + KS * it;
+      const bool active = tb < nt;
+      const int key0 = (blk0 + tb) * kBlockKeys;
+      if (active) stage(key0, T, kst, vst);
+      tile_sync<RT>();
+      if (tb + KS < nt) issue_target(tb + KS, kst, vst);
+      if (active) {
+        f32x16 sacc = {};
 #pragma unroll
-        for (int t = 0; t < 8; ++t) vcur[t] = u32x4{0u, 0u, 0u, 0u};
+        for (int kc = 0; kc < 8; ++kc) {
+          const u32x4 kraw = *(const u32x4*)(ktile + k_rd + kc * 16);
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kraw), qop[kc], sacc, 0, 0, 0);
+        }
+        uint32_t valid = 0xffffu;
+        if (key0 + kBlockKeys > T) {
+          valid = 0;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) valid |= (uint32_t)(key0 + 16 * (v >> 3) + 8 * hh + (v & 7) < T) << v;
+        }
+        softmax_pv(sacc, vtile, vt_off, valid, oacc, st);
       }
+      tile_sync<RT>();
     }
-    store_vt(vt, vcur, l32, hh);
-    wave_lds_sync();
-    bf16x8 kop[8];
-#pragma unroll
-    for (int kc = 0; kc < 8; ++kc) kop[kc] = as_bf16x8(kcur[kc]);
-    if (nblk < blk1) issue_loads(nblk, nA, nB, kcur, vcur);
-    uint32_t valid = 0xffffu;
-    if (tail) {
-      valid = 0;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) valid |= (uint32_t)(key0 + 16 * (v >> 3) + 8 * hh + (v & 7) < T) << v;
-    }
-    attend_block(kop, qop, vt, l32, hh, valid, oacc, st);
-    wave_lds_sync();
   }
 
-  // ---- draft blocks (last split only): keys 0..S-1 ----
-  if (last) {
-    const int nbd = (S + kBlockKeys - 1) / kBlockKeys;
-    int depth_k = 0;
-    for (int db = ks; db < nbd; db += KS) {
+  // ---- draft blocks (last split only): keys 0..S-1, rotated at their own positions ----
+  {
+    const int iters = (nd + KS - 1) / KS;
+    for (int it = 0; it < iters; ++it) {
+      const int db = ks + KS * it;
+      const bool active = db < nd;
       const int key0 = db * kBlockKeys;
-      const int ks_k = key0 + kperm;          // draft key behind this lane's K row
-      const int ks_v = key0 + l32;            // draft key behind this lane's V row
-      const int sk = ks_k < S ? ks_k : S - 1;
-      const int sv = ks_v < S ? ks_v : S - 1;
-      const uint16_t* kp = (const uint16_t*)p.draft_k + draft_offset(b, sk, h, p.max_draft, p.hkv) + hh * 8;
-      const uint16_t* vp = (const uint16_t*)p.draft_v + draft_offset(b, sv, h, p.max_draft, p.hkv) + hh * 8;
-      u32x4 kraw[8], vraw[8];
+      if (active) {
+        u32x4 kd[kLoadsPerWave], vd[kLoadsPerWave];
 #pragma unroll
-      for (int kc = 0; kc < 8; ++kc) kraw[kc] = *(const u32x4*)(kp + kc * 16);
-#pragma unroll
-      for (int t = 0; t < 8; ++t) vraw[t] = *(const u32x4*)(vp + t * 16);
-      if (ks_v >= S) {
-#pragma unroll
-        for (int t = 0; t < 8; ++t) vraw[t] = u32x4{0u, 0u, 0u, 0u};
+        for (int i = 0; i < kLoadsPerWave; ++i) {
+          int s = key0 + 4 * (rt + RT * i) + ld_row;
+          s = s < S ? s : S - 1;
+          const int64_t off = draft_offset(b, s, h, p.max_draft, p.hkv) + ld_chunk * 8;
+          kd[i] = *(const u32x4*)(dkbase + off);
+          vd[i] = *(const u32x4*)(dvbase + off);
+        }
+        stage(key0, S, kd, vd);
       }
-      int kpos;
-      if (p.tree) {
-        depth_k = __shfl(depth_mine, sk & 63);
-        kpos = T + depth_k;
-      } else {
-        kpos = T + sk;
-      }
-      kpos = kpos >= p.max_position ? p.max_position - 1 : kpos;
-      bf16x8 kop[8];
-      rope_rotate_to_bf16(kraw, p.rope + (int64_t)kpos * kHalfDim + hh * 8, 1.0f, kop);
-      store_vt(vt, vraw, l32, hh);
-      wave_lds_sync();
-      uint32_t valid = 0;
+      tile_sync<RT>();
+      if (active) {
+        u32x4 kraw[8];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int s = key0 + 16 * (v >> 3) + 8 * hh + (v & 7);
-        bool ok = s < S;
-        if (p.tree) ok = ok && ((row_anc >> (s & 63)) & 1ull);
-        else ok = ok && (s <= s0 + j);
-        valid |= (uint32_t)ok << v;
+        for (int kc = 0; kc < 8; ++kc) kraw[kc] = *(const u32x4*)(ktile + k_rd + kc * 16);
+        const int sk = min(key0 + kperm, S - 1);
+        int kpos = p.tree ? T + __shfl(depth_mine, sk & 63) : T + sk;
+        kpos = kpos >= p.max_position ? p.max_position - 1 : kpos;
+        bf16x8 kop[8];
+        rope_rotate_to_bf16(kraw, p.rope + (int64_t)kpos * kHalfDim + hh * 8, 1.0f, kop);
+        uint32_t valid = 0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int s = key0 + 16 * (v >> 3) + 8 * hh + (v & 7);
+          bool ok = s < S;
+          if (p.tree) ok = ok && ((row_anc >> (s & 63)) & 1ull);
+          else ok = ok && (s <= s0 + j);
+          valid |= (uint32_t)ok << v;
+        }
+        f32x16 sacc = {};
+#pragma unroll
+        for (int kc = 0; kc < 8; ++kc) sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qop[kc], sacc, 0, 0, 0);
+        softmax_pv(sacc, vtile, vt_off, valid, oacc, st);
       }
-      attend_block(kop, qop, vt, l32, hh, valid, oacc, st);
-      wave_lds_sync();
+      tile_sync<RT>();
     }
   }
 

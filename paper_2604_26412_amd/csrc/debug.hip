@@ -63,7 +63,40 @@ __global__ __launch_bounds__(256) void validate_kernel(AttnParams p, int max_ctx
   }
 }
 
+// Streaming read of `n16` 16-byte words with non-temporal loads: each lane
+// folds what it reads with xor so the loads cannot be dropped, and every
+// workgroup stores one word.  Used only to measure the device's practical
+// read bandwidth.
+typedef uint32_t sr_u32x4 __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(256) void stream_read_kernel(const sr_u32x4* __restrict__ src, int64_t n16,
+                                                          sr_u32x4* sink) {
+  const int64_t stride = (int64_t)gridDim.x * 256 * 8;
+  sr_u32x4 acc = {0, 0, 0, 0};
+  for (int64_t i = (int64_t)blockIdx.x * 256 * 8 + threadIdx.x; i < n16; i += stride) {
+    sr_u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = (i + u * 256 < n16) ? __builtin_nontemporal_load(src + i + u * 256) : sr_u32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u];
+  }
+  __shared__ sr_u32x4 red[256];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    sr_u32x4 r = {0, 0, 0, 0};
+    for (int k = 0; k < 256; ++k) r ^= red[k];
+    sink[blockIdx.x] = r;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int blocks, hipStream_t s) {
+  hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(256), 0, s, (const sr_u32x4*)src, bytes / 16,
+                     (sr_u32x4*)sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_gather_kv(const AttnParams& p, int max_ctx, void* k_dense, void* v_dense, int bf16,
                             hipStream_t s) {
