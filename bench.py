@@ -3,19 +3,20 @@
 
 Default workload: batch 64, target context 32768, 32 query / 8 KV heads,
 head_dim 128, k = 8 draft steps folded into one call, bf16, 16-token pages
-with a random page table.  One "step" is one call of the library (the
-attention kernel plus, with split-K, the combine kernel) over that batch.
+with a random page table.  One "step" is one pass of the whole path over that
+batch: the attention kernel plus, when the context is split, the combine
+kernel (``--mode sequential`` makes a step k calls of one draft query each).
 
 Prints one JSON line: effective HBM GB/s (algorithmic bytes / step time),
 draft tokens/s, the roofline of the dominant (attention) kernel, and the CPU
-oracle timed on a bounded sample of the same workload.
+oracle timed on a bounded sample of the same workload.  Other workloads
+(``--workload``) print the same fields.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
 import json
-import math
 import os
 import re
 import sys
@@ -26,6 +27,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
+METRIC = "draft-attention effective HBM GB/s (% of peak) + draft tokens/s at 32K ctx"
+DEFAULT_WORKLOAD = "long_b64_ctx32k_k8"
 
 
 def log(msg):
@@ -53,8 +56,12 @@ def read_traffic(workload: str, mode: str):
     return float(f.group(1)) + float(w.group(1))
 
 
+# ---------------------------------------------------------------------------
+# workloads on the device
+# ---------------------------------------------------------------------------
+
 def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=128, P=16):
-    """Seeded device-side generator for the 64 x 32768 workload (values N(0,1), bf16)."""
+    """Seeded device-side generator for the 64 x 32768 workload (values N(0,1), bf16, random page table)."""
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     pps = T // P
@@ -73,12 +80,31 @@ def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=1
     dv = torch.randn((B, n, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
     lens = torch.full((B,), T, dtype=torch.int32, device=dev)
     offs = torch.zeros((B,), dtype=torch.int32, device=dev)
-    return dict(q=q, k_pages=kp, v_pages=vp, page_table=table, ctx_lens=lens, draft_k=dk, draft_v=dv,
-                extra=offs, pool=pool, pps=pps, B=B, T=T, n=n, Hq=Hq, Hkv=Hkv, D=D, P=P)
+    return dict(mode="step", q=q, k_pages=kp, v_pages=vp, page_table=table, ctx_lens=lens, draft_k=dk, draft_v=dv,
+                extra=offs, pool=pool, pps=pps, B=B, n=n, Hq=Hq, Hkv=Hkv, D=D, P=P, max_draft=n,
+                lens=[T] * B, offsets=[0] * B, dtype="bf16", host=None, theta=1e6, scale=0.0)
 
 
-def host_sample(torch, d, seqs):
-    """Copy sequences `seqs` of a device workload into a compact host case (for the oracle)."""
+def upload_case(torch, case):
+    import numpy as np
+
+    def dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    B, n, Hq, D = case.q.shape
+    extra = case.step_offsets if case.mode == "step" else case.parents
+    return dict(mode=case.mode, q=dev(case.q), k_pages=dev(case.k_pages), v_pages=dev(case.v_pages),
+                page_table=dev(case.page_table), ctx_lens=dev(case.ctx_lens), draft_k=dev(case.draft_k),
+                draft_v=dev(case.draft_v), extra=dev(extra), pool=case.num_pages, pps=case.max_pages_per_seq, B=B,
+                n=n, Hq=Hq, Hkv=case.num_kv_heads, D=D, P=case.page_size, max_draft=case.max_draft,
+                lens=[int(x) for x in case.ctx_lens], dtype=case.dtype, host=case, theta=case.rope_theta,
+                scale=case.softmax_scale,
+                offsets=[int(x) for x in case.step_offsets] if case.mode == "step" else [0] * B)
+
+
+def host_sample_long(torch, d, seqs):
+    """Copy sequences `seqs` of the device-generated workload into a compact host case (for the oracle)."""
     import numpy as np
 
     import workloads as W
@@ -93,9 +119,24 @@ def host_sample(torch, d, seqs):
     pt = np.arange(ns * pps, dtype=np.int32).reshape(ns, pps)
     return W.DraftCase(mode="step", dtype="bf16", num_q_heads=d["Hq"], num_kv_heads=d["Hkv"], head_dim=d["D"],
                        page_size=d["P"], max_draft=d["n"], n_new=d["n"], q=bits(d["q"][seqs]), k_pages=kp,
-                       v_pages=vp, page_table=pt, ctx_lens=np.full(ns, d["T"], np.int32),
+                       v_pages=vp, page_table=pt, ctx_lens=np.array([d["lens"][s] for s in seqs], np.int32),
                        draft_k=bits(d["draft_k"][seqs]), draft_v=bits(d["draft_v"][seqs]),
                        step_offsets=np.zeros(ns, np.int32))
+
+
+# ---------------------------------------------------------------------------
+# byte accounting
+# ---------------------------------------------------------------------------
+
+def call_bytes(d, n_q, draft_seen):
+    """Algorithmic bytes of one call: target K/V once, page-table entries, q, draft K/V seen, out."""
+    eb = 2 if d["dtype"] == "bf16" else 4
+    row = d["Hkv"] * d["D"] * eb
+    kv = sum(2 * T * row for T in d["lens"])
+    pt = sum(-(-T // d["P"]) * 4 for T in d["lens"])
+    q = d["B"] * n_q * d["Hq"] * d["D"] * eb
+    dkv = sum(2 * s * row for s in draft_seen)
+    return kv + pt + q + dkv + q
 
 
 def blas_threads():
@@ -113,28 +154,59 @@ def cpu_baseline(torch, d, out_gpu, budget_s=15.0):
 
     import oracle
 
-    first = host_sample(torch, d, [0])
+    def sample(seqs):
+        if d["host"] is None:
+            return host_sample_long(torch, d, seqs), None
+        return d["host"], seqs
+
+    c0, s0 = sample([0])
     t0 = time.perf_counter()
-    ref0, _ = oracle.draft_attention(first)
+    ref0, _ = oracle.draft_attention(c0, seqs=s0)
     t1 = time.perf_counter() - t0
-    ns = int(max(1, min(8, budget_s // max(t1, 1e-3))))
-    seqs = list(range(1, 1 + ns))
-    case = host_sample(torch, d, seqs)
-    t0 = time.perf_counter()
-    ref, _ = oracle.draft_attention(case)
-    dt = time.perf_counter() - t0
-    per_seq_bytes = 2 * d["T"] * d["Hkv"] * d["D"] * 2 + 2 * d["n"] * d["Hkv"] * d["D"] * 2 + \
-        (d["T"] // d["P"]) * 4 + 2 * d["n"] * d["Hq"] * d["D"] * 2
+    if s0 is not None:
+        ref0 = ref0[[0]]
+    ns = int(max(0, min(8, d["B"] - 1, budget_s // max(t1, 1e-3))))
+    if ns == 0:                                    # one sequence: the first timing is the sample
+        seqs, ref, dt, ns_t, timed = [], ref0[:0], t1, 1, [0]
+    else:
+        seqs = list(range(1, 1 + ns))
+        c1, s1 = sample(seqs)
+        t0 = time.perf_counter()
+        ref, _ = oracle.draft_attention(c1, seqs=s1)
+        dt = time.perf_counter() - t0
+        if s1 is not None:
+            ref = ref[seqs]
+        ns_t, timed = ns, seqs
+    ns = ns_t
+    sub = dict(d, B=ns, lens=[d["lens"][s] for s in timed])
+    if d["mode"] == "step":
+        seen = [d["offsets"][s] + d["n"] for s in timed]
+    else:
+        seen = [d["n"]] * ns
+    nbytes = call_bytes(sub, d["n"], seen)
     got = out_gpu[[0] + seqs].float().cpu().numpy().astype(np.float64)
     allref = np.concatenate([ref0, ref], 0)
     diff = got - allref
     parity = dict(max_abs=float(np.abs(diff).max()),
                   rel_l2=float(np.linalg.norm(diff) / np.linalg.norm(allref)), sequences=1 + ns)
-    return dict(value=round(ns * per_seq_bytes / dt / 1e9, 4), unit="GB/s",
-                draft_tokens_per_s=round(ns * d["n"] / dt, 2), cores=blas_threads(), kind="oracle",
-                host_cpus=os.cpu_count(), seconds=round(dt, 3),
-                sample=f"{ns} whole sequence(s) (ctx {d['T']}, {d['n']} draft queries x {d['Hq']} heads) of the "
-                       f"same workload, float64 NumPy oracle"), parity
+    return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", draft_tokens_per_s=round(ns * d["n"] / dt, 2),
+                cores=blas_threads(), kind="oracle", host_cpus=os.cpu_count(), seconds=round(dt, 3),
+                sample=f"{ns} whole sequence(s) of the same workload ({d['n']} draft queries x {d['Hq']} heads each), "
+                       f"float64 NumPy oracle; value is the same algorithmic bytes per second"), parity
+
+
+def stream_ceiling(torch, K, tensor):
+    """Non-temporal streaming-read rate of the device over `tensor` (GB/s)."""
+    sink = torch.empty(4096 * 4, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        K.stream_read(tensor, sink, 4096)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        K.stream_read(tensor, sink, 4096)
+    e1.record()
+    torch.cuda.synchronize()
+    return tensor.numel() * tensor.element_size() / (e0.elapsed_time(e1) / 10 * 1e-3) / 1e9
 
 
 def main():
@@ -142,8 +214,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8"])
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--cold", action="store_true",
+                    help="flush the device caches (write 1 GiB) before every timed call; per-call events")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=1004)
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,
@@ -155,38 +231,57 @@ def main():
 
     import torch
 
-    from paper_2604_26412_amd import DraftAttention, OPT_PROFILE, OPT_SPLITS
+    import paper_2604_26412_amd as K
+    import workloads as W
+
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    log("generating the 64 x 32768 workload on the device")
-    d = make_long_range_on_device(torch, args.seed)
+    if args.workload == DEFAULT_WORKLOAD:
+        log("generating the 64 x 32768 workload on the device")
+        d = make_long_range_on_device(torch, args.seed)
+    else:
+        log(f"generating {args.workload} on the host")
+        d = upload_case(torch, W.workload(args.workload))
+    if d["mode"] == "tree" and args.mode == "sequential":
+        raise SystemExit("sequential mode applies to step workloads only")
     torch.cuda.synchronize()
-    B, T, n, Hq, Hkv, D, P = d["B"], d["T"], d["n"], d["Hq"], d["Hkv"], d["D"], d["P"]
-    att = DraftAttention(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=P, dtype="bf16", max_batch=B,
-                         max_draft=n, max_pages_per_seq=d["pps"], num_pages=d["pool"])
+    B, n, Hq, Hkv, D, P = d["B"], d["n"], d["Hq"], d["Hkv"], d["D"], d["P"]
+    T_max = max(d["lens"])
+    att = K.DraftAttention(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=P, dtype=d["dtype"],
+                           max_batch=B, max_draft=d["max_draft"], max_pages_per_seq=d["pps"], num_pages=d["pool"],
+                           rope_theta=d["theta"], softmax_scale=d["scale"])
     if args.splits:
-        att.set_option(OPT_SPLITS, args.splits)
-    plan = att.plan(B, n if args.mode == "folded" else 1, T)
-    out = torch.empty((B, n, Hq, D), dtype=torch.bfloat16, device="cuda")
+        att.set_option(K.OPT_SPLITS, args.splits)
+    nq_call = n if args.mode == "folded" else 1
+    plan = att.plan(B, nq_call, T_max)
+    edt = torch.bfloat16 if d["dtype"] == "bf16" else torch.float32
+    out = torch.empty((B, n, Hq, D), dtype=edt, device="cuda")
     stream = torch.cuda.current_stream()
 
-    if args.mode == "folded":
+    if d["mode"] == "tree":
+        def step():
+            att.tree(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["ctx_lens"], d["draft_k"], d["draft_v"],
+                     d["extra"], max_ctx=T_max, out=out)
+        draft_seen = [[n] * B]
+    elif args.mode == "folded":
         def step():
             att.step(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["ctx_lens"], d["draft_k"], d["draft_v"],
-                     d["extra"], max_ctx=T, out=out)
-        queries_per_step = B * n
-        calls_per_step = 1
+                     d["extra"], max_ctx=T_max, out=out)
+        draft_seen = [[o + n for o in d["offsets"]]]
     else:
         qs = [d["q"][:, j:j + 1].contiguous() for j in range(n)]
-        offs = [torch.full((B,), j, dtype=torch.int32, device="cuda") for j in range(n)]
-        outs = [torch.empty((B, 1, Hq, D), dtype=torch.bfloat16, device="cuda") for _ in range(n)]
+        offs = [(d["extra"] + j).contiguous() for j in range(n)]
+        outs = [torch.empty((B, 1, Hq, D), dtype=edt, device="cuda") for _ in range(n)]
 
         def step():
             for j in range(n):
                 att.step(qs[j], d["k_pages"], d["v_pages"], d["page_table"], d["ctx_lens"], d["draft_k"],
-                         d["draft_v"], offs[j], max_ctx=T, out=outs[j])
-        queries_per_step = B * n
-        calls_per_step = n
+                         d["draft_v"], offs[j], max_ctx=T_max, out=outs[j])
+        draft_seen = [[o + j + 1 for o in d["offsets"]] for j in range(n)]
+    step_bytes = sum(call_bytes(d, nq_call, seen) for seen in draft_seen)
+    # the attention kernel of the last call of a step; with split-K the combine writes the output
+    out_bytes = B * nq_call * Hq * D * (2 if d["dtype"] == "bf16" else 4)
+    attn_launch_bytes = call_bytes(d, nq_call, draft_seen[-1]) - (out_bytes if plan["splits"] > 1 else 0)
 
     if args.copy_calib_gib > 0:
         nbytes = int(args.copy_calib_gib * (1 << 30))
@@ -197,52 +292,61 @@ def main():
         torch.cuda.synchronize()
         log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
         del src, dst
+
     log(f"plan {plan}; warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    log(f"timing {args.steps} steps")
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = e0.elapsed_time(e1) / args.steps
+    log(f"timing {args.steps} steps" + (" (cold caches)" if args.cold else ""))
+    if args.cold:
+        flush = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+        times = []
+        for _ in range(args.steps):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        times.sort()
+        ms_per_step = times[len(times) // 2]
+        del flush
+    else:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = e0.elapsed_time(e1) / args.steps
 
     # per-kernel durations from HIP events the library records around each launch on this stream
-    att.set_option(OPT_PROFILE, 1)
+    att.set_option(K.OPT_PROFILE, 1)
     for _ in range(args.steps):
         step()
     prof = att.profile_read()
-    att.set_option(OPT_PROFILE, 0)
-    attn_ms = prof["attn_ms"] / max(1, prof["calls"])
-    comb_ms = prof["combine_ms"] / max(1, prof["calls"])
+    att.set_option(K.OPT_PROFILE, 0)
+    calls = max(1, prof["calls"])
+    attn_ms = prof["attn_ms"] / calls
+    comb_ms = prof["combine_ms"] / calls
     log(f"step {ms_per_step:.4f} ms; attention kernel {attn_ms:.4f} ms; combine {comb_ms:.4f} ms")
+    ceiling = stream_ceiling(torch, K, d["k_pages"])
+    log(f"non-temporal streaming-read ceiling {ceiling:.1f} GB/s")
 
-    nq_call = n if args.mode == "folded" else 1
-    # bytes one call must move: target K/V and page table once, q, the draft K/V rows it can see, out
-    kv_bytes = 2 * B * T * Hkv * D * 2 + B * (T // P) * 4
-    q_bytes = B * nq_call * Hq * D * 2
-    out_bytes = B * nq_call * Hq * D * 2
-    if args.mode == "folded":
-        dkv = [2 * B * n * Hkv * D * 2]
-    else:
-        dkv = [2 * B * (j + 1) * Hkv * D * 2 for j in range(n)]
-    step_bytes = sum(kv_bytes + q_bytes + x + out_bytes for x in dkv)
-    # the attention kernel of the last call of a step (the dominant kernel; the combine writes out when split)
-    attn_launch_bytes = kv_bytes + q_bytes + dkv[-1] + (out_bytes if plan["splits"] == 1 else 0)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     achieved = attn_launch_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = read_traffic("long_b64_ctx32k_k8", args.mode)
-
+    traffic = read_traffic(args.workload, args.mode) if not args.splits else None
+    path_name = {1: "attn_mfma_kernel", 2: "attn_generic_kernel"}[plan["path"]]
+    kernel = f"{path_name}<{plan['row_tiles']},{8 if plan['row_tiles'] >= 8 else 4}>" if plan["path"] == 1 \
+        else path_name
     res = {
-        "metric": "draft-attention effective HBM GB/s (% of peak) + draft tokens/s at 32K ctx",
+        "metric": METRIC,
         "value": round(value, 2),
         "unit": "GB/s",
         "pct_of_peak": round(100.0 * value / PEAK_HBM_GBS, 2),
-        "draft_tokens_per_s": round(queries_per_step / (ms_per_step * 1e-3), 1),
+        "draft_tokens_per_s": round(B * n / (ms_per_step * 1e-3), 1),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -250,24 +354,28 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": d["dtype"],
         "data": "synthetic",
-        "config": {"workload": f"long-range draft attention: batch {B}, ctx {T}, {Hq}/{Hkv} heads, head_dim {D}, "
-                               f"k={n} draft steps ({args.mode}), bf16, 16-token pages, random page table",
-                   "batch": B, "ctx_len": T, "draft_steps": n, "mode": args.mode, "page_size": P,
-                   "splits": plan["splits"], "workgroups": plan["workgroups"]},
+        "config": {"workload": f"{args.workload}: batch {B}, ctx {T_max if len(set(d['lens'])) == 1 else 'ragged'}, "
+                               f"{Hq}/{Hkv} heads, head_dim {D}, {n} draft "
+                               f"{'nodes (tree)' if d['mode'] == 'tree' else 'steps (' + args.mode + ')'}, "
+                               f"{d['dtype']}, {P}-token pages, random page table",
+                   "batch": B, "ctx_len_max": T_max, "draft_queries": n, "mode": args.mode if d["mode"] == "step"
+                   else "tree", "page_size": P, "splits": plan["splits"], "workgroups": plan["workgroups"],
+                   "cold_caches": bool(args.cold)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4),
-                     "traffic": traffic, "kernel": "attn_mfma_kernel<1,4>", "kernel_ms": round(attn_ms, 5),
-                     "combine_ms": round(comb_ms, 5), "algorithmic_bytes_per_launch": attn_launch_bytes},
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel,
+                     "kernel_ms": round(attn_ms, 5), "combine_ms": round(comb_ms, 5),
+                     "algorithmic_bytes_per_launch": attn_launch_bytes,
+                     "measured_stream_read_ceiling": round(ceiling, 1),
+                     "frac_of_measured_ceiling": round(achieved / ceiling, 4)},
         "whole_job_algorithmic_bytes": step_bytes,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.mode == "folded":
         log("timing the CPU oracle on a bounded sample")
-        if args.mode == "folded":
-            cb, parity = cpu_baseline(torch, d, out)
-            res["cpu_baseline"] = cb
-            res["parity_sample"] = parity
+        cb, parity = cpu_baseline(torch, d, out)
+        res["cpu_baseline"] = cb
+        res["parity_sample"] = parity
     print(json.dumps(res), flush=True)
     att.close()
 

@@ -88,10 +88,13 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
   if (c->opt_splits > 0) {
     splits = c->opt_splits;
   } else {
-    // One round of workgroups over the chip (two 4-wave or one 8-wave workgroup
-    // per CU are resident at once); split the context only when the (sequence,
-    // KV head) pairs alone leave CUs idle, and keep >= 4 blocks per wave.
-    const int target_wgs = c->num_cus * (8 / pl.waves_per_wg);
+    // One round of resident workgroups over the chip: split the context only
+    // when the (sequence, KV head) pairs alone leave CUs idle, and keep >= 4
+    // blocks per wave.  (Each workgroup starts with a dependent chain of
+    // loads -- length, page ids, K/V, RoPE table -- that only other resident
+    // workgroups can hide, so more, shorter workgroups lose.)
+    const int per_cu = generic ? 2 : mfma_wgs_per_cu(pl.row_tiles);
+    const int target_wgs = c->num_cus * per_cu;
     splits = (target_wgs + pairs - 1) / pairs;
     const int cap = nb / (pl.key_streams * 4);
     splits = splits > cap ? cap : splits;

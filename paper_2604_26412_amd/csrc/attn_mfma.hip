@@ -79,25 +79,70 @@ __device__ __forceinline__ void rope_rotate_to_bf16(const u32x4 (&raw)[8], const
   }
 }
 
+// Same rotation; the scaled query is kept as a bf16 pair hi + lo whose sum
+// carries ~16 mantissa bits, so the scores see almost none of its rounding.
+__device__ __forceinline__ void rope_rotate_split(const u32x4 (&raw)[8], const float2* cs, float scale,
+                                                  bf16x8 (&hi_out)[8], bf16x8 (&lo_out)[8]) {
+#pragma unroll
+  for (int kc = 0; kc < 4; ++kc) {
+    u32x4 h1, h2, l1, l2;
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2) {
+      const uint32_t a = raw[kc][e2], bq = raw[kc + 4][e2];
+      const float x1a = bf16_lo(a), x1b = bf16_hi(a);
+      const float x2a = bf16_lo(bq), x2b = bf16_hi(bq);
+      const float2 ca = cs[kc * 16 + 2 * e2], cb = cs[kc * 16 + 2 * e2 + 1];
+      const float y1a = (x1a * ca.x - x2a * ca.y) * scale, y1b = (x1b * cb.x - x2b * cb.y) * scale;
+      const float y2a = (x2a * ca.x + x1a * ca.y) * scale, y2b = (x2b * cb.x + x1b * cb.y) * scale;
+      h1[e2] = pack_bf16x2(y1a, y1b);
+      h2[e2] = pack_bf16x2(y2a, y2b);
+      l1[e2] = pack_bf16x2(y1a - bf16_lo(h1[e2]), y1b - bf16_hi(h1[e2]));
+      l2[e2] = pack_bf16x2(y2a - bf16_lo(h2[e2]), y2b - bf16_hi(h2[e2]));
+    }
+    hi_out[kc] = as_bf16x8(h1);
+    hi_out[kc + 4] = as_bf16x8(h2);
+    lo_out[kc] = as_bf16x8(l1);
+    lo_out[kc + 4] = as_bf16x8(l2);
+  }
+}
+
 struct SoftmaxState {
   float m;   // running max (log2 units), identical in both lane halves
   float l;   // this lane's partial sum over its keys
 };
 
+// A row's reference max only moves when a block's max exceeds it by more
+// than this (log2 units): weights stay <= 2^8, and the output accumulator is
+// rescaled only for the few blocks where some row's max jumps.  The final
+// normalisation divides by the sum taken against the same reference, so the
+// result is the same softmax.
+constexpr float kRescaleSlack = 8.0f;
+
 // Softmax update and O^T += V^T P^T for one block whose scores are in `s`.
-// `valid` bit v: key of accumulator register v is visible to this lane's row.
-__device__ __forceinline__ void softmax_pv(f32x16 s, const uint16_t* vtile, int vt_off, uint32_t valid,
+// When `masked`, bit v of `valid` says whether the key of accumulator register
+// v is visible to this lane's row.
+__device__ __forceinline__ void softmax_pv(f32x16 s, const uint16_t* vtile, int vt_off, bool masked, uint32_t valid,
                                            f32x16 (&oacc)[4], SoftmaxState& st) {
   float bm = -INFINITY;
+  if (masked) {
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    s[v] = ((valid >> v) & 1u) ? s[v] : -INFINITY;
-    bm = fmaxf(bm, s[v]);
+    for (int v = 0; v < 16; ++v) s[v] = ((valid >> v) & 1u) ? s[v] : -INFINITY;
   }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) bm = fmaxf(bm, s[v]);
   bm = fmaxf(bm, __shfl_xor(bm, 32));
-  const float mn = fmaxf(st.m, bm);
-  const float mu = mn == -INFINITY ? 0.0f : mn;
-  const float alpha = __builtin_amdgcn_exp2f(st.m - mu);
+  const bool jump = bm > st.m + kRescaleSlack;   // false while both are -inf
+  if (__any(jump)) {
+    const float mn = jump ? bm : st.m;
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mn);   // 0 when the old max was -inf
+    st.l *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
+    st.m = mn;
+  }
+  const float mu = st.m == -INFINITY ? 0.0f : st.m;
   float ps = 0.0f;
   u32x4 pw[2];
 #pragma unroll
@@ -107,14 +152,7 @@ __device__ __forceinline__ void softmax_pv(f32x16 s, const uint16_t* vtile, int 
     ps += p0 + p1;
     pw[v >> 3][(v & 7) >> 1] = pack_bf16x2(p0, p1);
   }
-  st.l = st.l * alpha + ps;
-  st.m = mn;
-  if (__any(alpha != 1.0f)) {
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
-  }
+  st.l += ps;
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
   const __attribute__((address_space(3))) uint16_t* vb =
       (const __attribute__((address_space(3))) uint16_t*)(vtile) + vt_off;
@@ -145,16 +183,16 @@ __device__ __forceinline__ void tile_sync() {
   }
 }
 
-#ifndef KVSHOT_MFMA_WAVES_PER_SIMD
-#define KVSHOT_MFMA_WAVES_PER_SIMD 2
-#endif
-
-template <int RT, int NW>
-__global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma_kernel(AttnParams p) {
+// RT: 32-row query tiles; NW: waves per workgroup; PF: blocks of K/V in
+// flight per wave (register staging ring); QSPLIT: query kept as a bf16 hi/lo
+// pair (two QK^T products); WPS: waves per SIMD the register budget allows.
+template <int RT, int NW, int PF, bool QSPLIT, int WPS>
+__global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   constexpr int KS = NW / RT;
   constexpr int kLoadsPerWave = 8 / RT;   // 16-byte load instructions per K (and per V) tile and wave
   constexpr int kMergeBytes = (KS - 1) * RT * 64 * (64 * 4 + 8);
-  constexpr int kTileBytes = KS * kStreamBytes;
+  constexpr int kBufs = RT > 1 ? 2 : 1;            // waves that share tiles double-buffer them
+  constexpr int kTileBytes = KS * kBufs * kStreamBytes;
   constexpr int kLdsBytes = kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
 
@@ -204,16 +242,29 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
 
   // ---- query operand: rotated, scaled into log2 units, bf16 ----
   bf16x8 qop[8];
+  bf16x8 qlo[QSPLIT ? 8 : 1];
   {
     const uint16_t* qp = (const uint16_t*)p.q + (((int64_t)b * p.nq + j) * p.hq + hq) * kHeadDim + hh * 8;
     u32x4 raw[8];
 #pragma unroll
     for (int kc = 0; kc < 8; ++kc) raw[kc] = *(const u32x4*)(qp + kc * 16);
-    rope_rotate_to_bf16(raw, p.rope + (int64_t)qpos * kHalfDim + hh * 8, row_ok ? p.qscale : 0.0f, qop);
+    const float2* cs = p.rope + (int64_t)qpos * kHalfDim + hh * 8;
+    if constexpr (QSPLIT) rope_rotate_split(raw, cs, row_ok ? p.qscale : 0.0f, qop, qlo);
+    else rope_rotate_to_bf16(raw, cs, row_ok ? p.qscale : 0.0f, qop);
   }
+  // S^T = K Q^T over the 8 operand chunks (and K Q_lo^T when the query is split)
+  auto qk = [&](const bf16x8 (&kop)[8]) {
+    f32x16 acc = {};
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qop[kc], acc, 0, 0, 0);
+      if constexpr (QSPLIT) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qlo[kc], acc, 0, 0, 0);
+    }
+    return acc;
+  };
 
-  uint16_t* ktile = (uint16_t*)(lds + ks * kStreamBytes);
-  uint16_t* vtile = (uint16_t*)(lds + ks * kStreamBytes + kKTileBytes);
+  uint16_t* ktile = (uint16_t*)(lds + ks * kBufs * kStreamBytes);
+  uint16_t* vtile = (uint16_t*)(lds + ks * kBufs * kStreamBytes + kKTileBytes);
 
   // K-operand row rho = l32 reads tile row kperm(rho), chosen so that
   // accumulator register v of lane (row, hh) holds key 16 * (v / 8) + 8 * hh + v % 8.
@@ -242,6 +293,9 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
   const int64_t pt_row = (int64_t)b * p.max_pages_per_seq;
 
   // Issue this wave's share of the loads of target block tb into kd / vd.
+  // Rows 0..15 and 16..31 of a block each lie in one page (P >= 16); their
+  // base addresses are wave-uniform, and a lane adds a small 32-bit offset.
+  const uint32_t sstr_b = (uint32_t)(sstr * 2);
   auto issue_target = [&](int tb, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
     const int key0 = (blk0 + tb) * kBlockKeys;
     int la = key0 >> p.page_shift, lb = (key0 + 16) >> p.page_shift;
@@ -251,57 +305,109 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
     int pb = load_scalar_i32(p.page_table, pt_row + lb);
     pa = pa < 0 ? 0 : (pa >= p.num_pages ? p.num_pages - 1 : pa);
     pb = pb < 0 ? 0 : (pb >= p.num_pages ? p.num_pages - 1 : pb);
+    const int64_t ea = (int64_t)pa * pstr + h * hstr + (int64_t)(key0 & pmask) * sstr;
+    const int64_t eb = (int64_t)pb * pstr + h * hstr + (int64_t)((key0 + 16) & pmask) * sstr;
+    const char* ka = (const char*)(kbase + ea);
+    const char* kb = (const char*)(kbase + eb);
+    const char* va = (const char*)(vbase + ea);
+    const char* vb2 = (const char*)(vbase + eb);
 #pragma unroll
     for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int t = rt + RT * i;                  // load instruction index within the block
-      const int kr = 4 * t + ld_row;             // key within the block
-      const int pid = kr >= 16 ? pb : pa;        // page sizes >= 32 have pa == pb
-      const int64_t off = kv_offset(pid, h, (key0 + kr) & pmask, pstr, hstr, sstr) + ld_chunk * 8;
+      const int t = rt + RT * i;                  // load instruction index: rows 4t .. 4t+3
+      const uint32_t off = (uint32_t)(4 * (t & 3) + ld_row) * sstr_b + (uint32_t)ld_chunk * 16u;
       // the prefix K/V is read exactly once: whole lines, non-temporal
-      kd[i] = __builtin_nontemporal_load((const u32x4*)(kbase + off));
-      vd[i] = __builtin_nontemporal_load((const u32x4*)(vbase + off));
+      kd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? kb : ka) + off));
+      vd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? vb2 : va) + off));
     }
   };
   // Stage this wave's share of a block into the LDS tiles; rows at or past
   // `kend` get zero V so masked weights never meet NaN.
-  auto stage = [&](int key0, int kend, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
+  auto stage = [&](int key0, int kend, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave], int buf) {
+    if (key0 + kBlockKeys > kend) {
+#pragma unroll
+      for (int i = 0; i < kLoadsPerWave; ++i)
+        if (key0 + 4 * (rt + RT * i) + ld_row >= kend) vd[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+    uint16_t* kt = ktile + buf * (kStreamBytes / 2);
+    uint16_t* vt = vtile + buf * (kStreamBytes / 2);
 #pragma unroll
     for (int i = 0; i < kLoadsPerWave; ++i) {
       const int kr = 4 * (rt + RT * i) + ld_row;
-      if (key0 + kr >= kend) vd[i] = u32x4{0u, 0u, 0u, 0u};
-      *(u32x4*)(ktile + kr * kKPitch + ld_chunk * 8) = kd[i];
-      *(u32x4*)(vtile + kr * kVPitch + ld_chunk * 8) = vd[i];
+      *(u32x4*)(kt + kr * kKPitch + ld_chunk * 8) = kd[i];
+      *(u32x4*)(vt + kr * kVPitch + ld_chunk * 8) = vd[i];
     }
   };
+  // QK^T, masking and the softmax / PV update for a staged target block
+  auto compute_target = [&](int key0, int buf) {
+    const uint16_t* kt = ktile + buf * (kStreamBytes / 2);
+    const uint16_t* vt = vtile + buf * (kStreamBytes / 2);
+    bf16x8 kop[8];
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc) kop[kc] = as_bf16x8(*(const u32x4*)(kt + k_rd + kc * 16));
+    const f32x16 sacc = qk(kop);
+    const bool masked = key0 + kBlockKeys > T;
+    uint32_t valid = 0xffffu;
+    if (masked) {
+      valid = 0;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) valid |= (uint32_t)(key0 + 16 * (v >> 3) + 8 * hh + (v & 7) < T) << v;
+    }
+    softmax_pv(sacc, vt, vt_off, masked, valid, oacc, st);
+  };
 
-  // ---- target blocks: tb = ks + KS * it, software-pipelined one block ahead ----
+  // ---- target blocks: tb = ks + KS * it, software-pipelined PF blocks ahead ----
+  // (a wave's share of a block is 8 / RT load instructions, so waves that
+  // share their tiles with others keep more blocks in flight)
   {
     const int iters = (nt + KS - 1) / KS;          // same for every wave of the workgroup
-    u32x4 kst[kLoadsPerWave], vst[kLoadsPerWave];
-    if (ks < nt) issue_target(ks, kst, vst);
-    for (int it = 0; it < iters; ++it) {
-      const int tb = ks + KS * it;
-      const bool active = tb < nt;
-      const int key0 = (blk0 + tb) * kBlockKeys;
-      if (active) stage(key0, T, kst, vst);
-      tile_sync<RT>();
-      if (tb + KS < nt) issue_target(tb + KS, kst, vst);
-      if (active) {
-        f32x16 sacc = {};
+    u32x4 kst[PF][kLoadsPerWave], vst[PF][kLoadsPerWave];
 #pragma unroll
-        for (int kc = 0; kc < 8; ++kc) {
-          const u32x4 kraw = *(const u32x4*)(ktile + k_rd + kc * 16);
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kraw), qop[kc], sacc, 0, 0, 0);
-        }
-        uint32_t valid = 0xffffu;
-        if (key0 + kBlockKeys > T) {
-          valid = 0;
+    for (int u = 0; u < PF; ++u)
+      if (ks + KS * u < nt) issue_target(ks + KS * u, kst[u], vst[u]);
+    if constexpr (RT == 1) {
+      // private tiles: stage block it from ring slot it % PF, refill the slot
+      // with block it + PF, compute (wave-local ordering only)
+      for (int it0 = 0; it0 < iters; it0 += PF) {
 #pragma unroll
-          for (int v = 0; v < 16; ++v) valid |= (uint32_t)(key0 + 16 * (v >> 3) + 8 * hh + (v & 7) < T) << v;
+        for (int u = 0; u < PF; ++u) {
+          const int it = it0 + u;
+          if (it < iters) {
+            const int tb = ks + KS * it;
+            const bool active = tb < nt;
+            const int key0 = (blk0 + tb) * kBlockKeys;
+            if (active) stage(key0, T, kst[u], vst[u], 0);
+            tile_sync<RT>();
+            if (tb + KS * PF < nt) issue_target(tb + KS * PF, kst[u], vst[u]);
+            if (active) compute_target(key0, 0);
+            tile_sync<RT>();
+          }
         }
-        softmax_pv(sacc, vtile, vt_off, valid, oacc, st);
       }
-      tile_sync<RT>();
+    } else {
+      // shared, double-buffered tiles: one barrier per block.  Block it is
+      // computed from buffer it % 2 while block it + 1 is staged into the
+      // other one (last read before the previous barrier).
+      if (iters > 0) {
+        if (ks < nt) stage((blk0 + ks) * kBlockKeys, T, kst[0], vst[0], 0);
+        if (ks + KS * PF < nt) issue_target(ks + KS * PF, kst[0], vst[0]);
+        __syncthreads();
+      }
+      for (int it0 = 0; it0 < iters; it0 += PF) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+          const int it = it0 + u;
+          if (it < iters) {
+            const int tb = ks + KS * it;
+            if (tb < nt) compute_target((blk0 + tb) * kBlockKeys, u & 1);
+            const int nb = tb + KS;                // next block: its loads sit in ring slot (u + 1) % PF
+            if (nb < nt) {
+              stage((blk0 + nb) * kBlockKeys, T, kst[(u + 1) % PF], vst[(u + 1) % PF], (u + 1) & 1);
+              if (nb + KS * PF < nt) issue_target(nb + KS * PF, kst[(u + 1) % PF], vst[(u + 1) % PF]);
+            }
+            __syncthreads();
+          }
+        }
+      }
     }
   }
 
@@ -322,7 +428,7 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
           kd[i] = *(const u32x4*)(dkbase + off);
           vd[i] = *(const u32x4*)(dvbase + off);
         }
-        stage(key0, S, kd, vd);
+        stage(key0, S, kd, vd, 0);
       }
       tile_sync<RT>();
       if (active) {
@@ -343,10 +449,7 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
           else ok = ok && (s <= s0 + j);
           valid |= (uint32_t)ok << v;
         }
-        f32x16 sacc = {};
-#pragma unroll
-        for (int kc = 0; kc < 8; ++kc) sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kc], qop[kc], sacc, 0, 0, 0);
-        softmax_pv(sacc, vtile, vt_off, valid, oacc, st);
+        softmax_pv(qk(kop), vtile, vt_off, true, valid, oacc, st);
       }
       tile_sync<RT>();
     }
@@ -434,15 +537,37 @@ __global__ __launch_bounds__(NW * 64, KVSHOT_MFMA_WAVES_PER_SIMD) void attn_mfma
 
 }  // namespace
 
+// Per row-tile configuration (waves per SIMD, blocks in flight, query split).
+#ifndef KVSHOT_RT1_WPS
+#define KVSHOT_RT1_WPS 1
+#endif
+#ifndef KVSHOT_RT1_PF
+#define KVSHOT_RT1_PF 1
+#endif
+#ifndef KVSHOT_QSPLIT_MAX_RT
+#define KVSHOT_QSPLIT_MAX_RT 1
+#endif
+
 int mfma_waves_per_wg(int row_tiles) { return row_tiles >= 8 ? 8 : 4; }
+
+// Workgroups of the kernel for `row_tiles` that one CU (4 SIMDs) holds at once.
+int mfma_wgs_per_cu(int row_tiles) {
+  const int wps = row_tiles == 1 ? KVSHOT_RT1_WPS : 2;
+  const int wgs = 4 * wps / mfma_waves_per_wg(row_tiles);
+  return wgs < 1 ? 1 : wgs;
+}
 
 hipError_t launch_attn_mfma(const AttnParams& p, int row_tiles, hipStream_t s) {
   const dim3 grid(p.splits, p.hkv, p.batch);
+  constexpr bool q1 = KVSHOT_QSPLIT_MAX_RT >= 1, q2 = KVSHOT_QSPLIT_MAX_RT >= 2, q4 = KVSHOT_QSPLIT_MAX_RT >= 4,
+                 q8 = KVSHOT_QSPLIT_MAX_RT >= 8;
   switch (row_tiles) {
-    case 1: hipLaunchKernelGGL((attn_mfma_kernel<1, 4>), grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((attn_mfma_kernel<2, 4>), grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((attn_mfma_kernel<4, 4>), grid, dim3(256), 0, s, p); break;
-    case 8: hipLaunchKernelGGL((attn_mfma_kernel<8, 8>), grid, dim3(512), 0, s, p); break;
+    case 1:
+      hipLaunchKernelGGL((attn_mfma_kernel<1, 4, KVSHOT_RT1_PF, q1, KVSHOT_RT1_WPS>), grid, dim3(256), 0, s, p);
+      break;
+    case 2: hipLaunchKernelGGL((attn_mfma_kernel<2, 4, 2, q2, 2>), grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((attn_mfma_kernel<4, 4, 2, q4, 2>), grid, dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL((attn_mfma_kernel<8, 8, 4, q8, 2>), grid, dim3(512), 0, s, p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

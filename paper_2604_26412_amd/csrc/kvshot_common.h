@@ -136,4 +136,5 @@ hipError_t launch_tree_mask(const int32_t* parents, int batch, int n, uint64_t* 
 hipError_t launch_validate(const AttnParams& p, int max_ctx_hint, int32_t* flag, hipStream_t s);
 hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int blocks, hipStream_t s);
 int mfma_waves_per_wg(int row_tiles);
+int mfma_wgs_per_cu(int row_tiles);
 }  // namespace kvshot
