@@ -220,6 +220,8 @@ def main():
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--cold", action="store_true",
                     help="flush the device caches (write 1 GiB) before every timed call; per-call events")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch each step from Python instead of replaying a captured HIP graph of it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=1004)
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,
@@ -297,6 +299,23 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run_step = step
+    if not args.no_graph:
+        # capture one step (every kernel launch of the path) in a HIP graph and replay it
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        for _ in range(args.warmup):
+            run_step()
+        torch.cuda.synchronize()
     log(f"timing {args.steps} steps" + (" (cold caches)" if args.cold else ""))
     if args.cold:
         flush = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
@@ -305,7 +324,7 @@ def main():
             flush.fill_(1)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            step()
+            run_step()
             e1.record(stream)
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1))
@@ -317,7 +336,7 @@ def main():
         torch.cuda.synchronize()
         e0.record(stream)
         for _ in range(args.steps):
-            step()
+            run_step()
         e1.record(stream)
         torch.cuda.synchronize()
         ms_per_step = e0.elapsed_time(e1) / args.steps
@@ -362,7 +381,7 @@ def main():
                                f"{d['dtype']}, {P}-token pages, random page table",
                    "batch": B, "ctx_len_max": T_max, "draft_queries": n, "mode": args.mode if d["mode"] == "step"
                    else "tree", "page_size": P, "splits": plan["splits"], "workgroups": plan["workgroups"],
-                   "cold_caches": bool(args.cold)},
+                   "cold_caches": bool(args.cold), "launch": "python" if args.no_graph else "hip graph replay"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel,
                      "kernel_ms": round(attn_ms, 5), "combine_ms": round(comb_ms, 5),

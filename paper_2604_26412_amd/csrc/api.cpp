@@ -55,7 +55,9 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Plan {
   int path;        // 1 mfma, 2 generic
-  int row_tiles;   // 32-row tiles (mfma) or 16-row tiles (generic, informational)
+  int row_tiles;   // 32-row query tiles per (sequence, KV head)
+  int kernel_row_tiles;  // of which one workgroup holds (row_groups = row_tiles / kernel_row_tiles)
+  int row_groups;
   int key_streams;
   int splits;
   int blocks_per_split;
@@ -76,14 +78,18 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
   pl.row_tiles = round_tiles(pl.rows);
   pl.rows_pad = pl.row_tiles * 32;
   if (generic) {
+    pl.kernel_row_tiles = pl.row_tiles;
+    pl.row_groups = 1;
     pl.waves_per_wg = 4;
     pl.key_streams = 1;
   } else {
-    pl.waves_per_wg = mfma_waves_per_wg(pl.row_tiles);
-    pl.key_streams = pl.waves_per_wg / pl.row_tiles;
+    pl.kernel_row_tiles = mfma_kernel_row_tiles(pl.row_tiles);
+    pl.row_groups = pl.row_tiles / pl.kernel_row_tiles;
+    pl.waves_per_wg = mfma_waves_per_wg(pl.kernel_row_tiles);
+    pl.key_streams = pl.waves_per_wg / pl.kernel_row_tiles;
   }
   const int nb = (max_ctx + kBlockKeys - 1) / kBlockKeys;
-  const int pairs = batch * c->cfg.num_kv_heads;
+  const int pairs = batch * c->cfg.num_kv_heads * pl.row_groups;   // workgroups per split
   int splits;
   if (c->opt_splits > 0) {
     splits = c->opt_splits;
@@ -93,7 +99,7 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
     // blocks per wave.  (Each workgroup starts with a dependent chain of
     // loads -- length, page ids, K/V, RoPE table -- that only other resident
     // workgroups can hide, so more, shorter workgroups lose.)
-    const int per_cu = generic ? 2 : mfma_wgs_per_cu(pl.row_tiles);
+    const int per_cu = generic ? 2 : mfma_wgs_per_cu(pl.kernel_row_tiles);
     const int target_wgs = c->num_cus * per_cu;
     splits = (target_wgs + pairs - 1) / pairs;
     const int cap = nb / (pl.key_streams * 4);
@@ -139,6 +145,7 @@ void fill_params(const kvshot_ctx* c, const Plan& pl, int batch, int nq, int max
   p.max_draft = g.max_draft;
   p.rows = pl.rows;
   p.rows_pad = pl.rows_pad;
+  p.row_groups = pl.row_groups;
   p.splits = pl.splits;
   p.blocks_per_split = pl.blocks_per_split;
   p.max_ctx = max_ctx;
@@ -214,7 +221,7 @@ kvshot_status run_call(kvshot_ctx* c, int batch, int nq, int max_ctx, bool tree,
     slot = &c->prof[c->prof_head % kProfileRing];
     if (hipEventRecord(slot->ev[0], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   }
-  hipError_t e = pl.path == 1 ? launch_attn_mfma(p, pl.row_tiles, s)
+  hipError_t e = pl.path == 1 ? launch_attn_mfma(p, pl.kernel_row_tiles, s)
                               : launch_attn_generic(p, g.dtype == KVSHOT_BF16, s);
   if (e != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (slot && hipEventRecord(slot->ev[1], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
@@ -438,7 +445,7 @@ kvshot_status kvshot_draft_attn_plan(kvshot_handle h, int32_t batch, int32_t n_q
   if (splits) *splits = pl.splits;
   if (path) *path = pl.path;
   if (row_tiles) *row_tiles = pl.row_tiles;
-  if (workgroups) *workgroups = pl.splits * h->cfg.num_kv_heads * batch;
+  if (workgroups) *workgroups = pl.splits * pl.row_groups * h->cfg.num_kv_heads * batch;
   return KVSHOT_OK;
 }
 

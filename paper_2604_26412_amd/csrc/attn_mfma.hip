@@ -202,7 +202,13 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   const int ks = w / RT;
   const int l32 = lane & 31;
   const int hh = lane >> 5;
-  const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int wi = xcd_remap(blockIdx.x, gridDim.x);       // work item: (row group, split, KV head, sequence)
+  const int rg = wi % p.row_groups;
+  wi /= p.row_groups;
+  const int split = wi % p.splits;
+  wi /= p.splits;
+  const int h = wi % p.hkv;
+  const int b = wi / p.hkv;
 
   int T = clamp_ctx(p.ctx_lens[b], p.max_pages_per_seq, p.page_shift);
   T = T > p.max_ctx ? p.max_ctx : T;
@@ -220,8 +226,67 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   }
   const int nd = last ? (S + kBlockKeys - 1) / kBlockKeys : 0;
 
+  uint16_t* ktile = (uint16_t*)(lds + ks * kBufs * kStreamBytes);
+  uint16_t* vtile = (uint16_t*)(lds + ks * kBufs * kStreamBytes + kKTileBytes);
+
+  // K-operand row rho = l32 reads tile row kperm(rho), chosen so that
+  // accumulator register v of lane (row, hh) holds key 16 * (v / 8) + 8 * hh + v % 8.
+  const int kperm = ((l32 >> 4) << 4) + (((l32 >> 2) & 1) << 3) + (((l32 >> 3) & 1) << 2) + (l32 & 3);
+  const int k_rd = kperm * kKPitch + hh * 8;
+  // transpose-read base: 16-lane group gr reads keys 8*(gr/2) + (lane%16)/4 of
+  // channels 16*(gr%2) + 4*(lane%4) .. +3; lane i of the group receives channel
+  // 16*(gr%2) + i of four consecutive keys
+  const int gr = lane >> 4, sg = lane & 15;
+  const int vt_off = ((gr >> 1) * 8 + (sg >> 2)) * kVPitch + (gr & 1) * 16 + 4 * (sg & 3);
+  // coalesced load / LDS write slot of this lane in load instruction t: row 4t + lane/16, 16-byte chunk lane%16
+  const int ld_row = lane >> 4, ld_chunk = lane & 15;
+
+  const int64_t pstr = p.page_stride, hstr = p.head_stride, sstr = p.slot_stride;
+  const uint16_t* kbase = (const uint16_t*)p.k_pages;
+  const uint16_t* vbase = (const uint16_t*)p.v_pages;
+  const uint16_t* dkbase = (const uint16_t*)p.draft_k;
+  const uint16_t* dvbase = (const uint16_t*)p.draft_v;
+  const int pmask = (1 << p.page_shift) - 1;
+  const int lp_last = T > 0 ? (T - 1) >> p.page_shift : 0;
+  const int64_t pt_row = (int64_t)b * p.max_pages_per_seq;
+
+  // Issue this wave's share of the loads of target block tb into kd / vd.
+  // Rows 0..15 and 16..31 of a block each lie in one page (P >= 16); their
+  // base addresses are wave-uniform, and a lane adds a small 32-bit offset.
+  const uint32_t sstr_b = (uint32_t)(sstr * 2);
+  auto issue_target = [&](int tb, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
+    const int key0 = (blk0 + tb) * kBlockKeys;
+    int la = key0 >> p.page_shift, lb = (key0 + 16) >> p.page_shift;
+    la = la > lp_last ? lp_last : la;
+    lb = lb > lp_last ? lp_last : lb;
+    int pa = load_scalar_i32(p.page_table, pt_row + la);
+    int pb = load_scalar_i32(p.page_table, pt_row + lb);
+    pa = pa < 0 ? 0 : (pa >= p.num_pages ? p.num_pages - 1 : pa);
+    pb = pb < 0 ? 0 : (pb >= p.num_pages ? p.num_pages - 1 : pb);
+    const int64_t ea = (int64_t)pa * pstr + h * hstr + (int64_t)(key0 & pmask) * sstr;
+    const int64_t eb = (int64_t)pb * pstr + h * hstr + (int64_t)((key0 + 16) & pmask) * sstr;
+    const char* ka = (const char*)(kbase + ea);
+    const char* kb = (const char*)(kbase + eb);
+    const char* va = (const char*)(vbase + ea);
+    const char* vb2 = (const char*)(vbase + eb);
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int t = rt + RT * i;                  // load instruction index: rows 4t .. 4t+3
+      const uint32_t off = (uint32_t)(4 * (t & 3) + ld_row) * sstr_b + (uint32_t)ld_chunk * 16u;
+      // the prefix K/V is read exactly once: whole lines, non-temporal
+      kd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? kb : ka) + off));
+      vd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? vb2 : va) + off));
+    }
+  };
+  // Start the K/V stream before the query setup so the two dependent load
+  // chains of the prologue overlap.
+  u32x4 kst[PF][kLoadsPerWave], vst[PF][kLoadsPerWave];
+#pragma unroll
+  for (int u = 0; u < PF; ++u)
+    if (ks + KS * u < nt) issue_target(ks + KS * u, kst[u], vst[u]);
+
   // query row of this lane
-  const int r = rt * 32 + l32;
+  const int r = (rg * RT + rt) * 32 + l32;
   const bool row_ok = r < p.rows;
   const int rr = row_ok ? r : p.rows - 1;
   const int j = rr / p.group;
@@ -263,63 +328,11 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
     return acc;
   };
 
-  uint16_t* ktile = (uint16_t*)(lds + ks * kBufs * kStreamBytes);
-  uint16_t* vtile = (uint16_t*)(lds + ks * kBufs * kStreamBytes + kKTileBytes);
-
-  // K-operand row rho = l32 reads tile row kperm(rho), chosen so that
-  // accumulator register v of lane (row, hh) holds key 16 * (v / 8) + 8 * hh + v % 8.
-  const int kperm = ((l32 >> 4) << 4) + (((l32 >> 2) & 1) << 3) + (((l32 >> 3) & 1) << 2) + (l32 & 3);
-  const int k_rd = kperm * kKPitch + hh * 8;
-  // transpose-read base: 16-lane group gr reads keys 8*(gr/2) + (lane%16)/4 of
-  // channels 16*(gr%2) + 4*(lane%4) .. +3; lane i of the group receives channel
-  // 16*(gr%2) + i of four consecutive keys
-  const int gr = lane >> 4, sg = lane & 15;
-  const int vt_off = ((gr >> 1) * 8 + (sg >> 2)) * kVPitch + (gr & 1) * 16 + 4 * (sg & 3);
-  // coalesced load / LDS write slot of this lane in load instruction t: row 4t + lane/16, 16-byte chunk lane%16
-  const int ld_row = lane >> 4, ld_chunk = lane & 15;
-
   f32x16 oacc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) oacc[dt] = f32x16{};
   SoftmaxState st{-INFINITY, 0.0f};
 
-  const int64_t pstr = p.page_stride, hstr = p.head_stride, sstr = p.slot_stride;
-  const uint16_t* kbase = (const uint16_t*)p.k_pages;
-  const uint16_t* vbase = (const uint16_t*)p.v_pages;
-  const uint16_t* dkbase = (const uint16_t*)p.draft_k;
-  const uint16_t* dvbase = (const uint16_t*)p.draft_v;
-  const int pmask = (1 << p.page_shift) - 1;
-  const int lp_last = T > 0 ? (T - 1) >> p.page_shift : 0;
-  const int64_t pt_row = (int64_t)b * p.max_pages_per_seq;
-
-  // Issue this wave's share of the loads of target block tb into kd / vd.
-  // Rows 0..15 and 16..31 of a block each lie in one page (P >= 16); their
-  // base addresses are wave-uniform, and a lane adds a small 32-bit offset.
-  const uint32_t sstr_b = (uint32_t)(sstr * 2);
-  auto issue_target = [&](int tb, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave]) {
-    const int key0 = (blk0 + tb) * kBlockKeys;
-    int la = key0 >> p.page_shift, lb = (key0 + 16) >> p.page_shift;
-    la = la > lp_last ? lp_last : la;
-    lb = lb > lp_last ? lp_last : lb;
-    int pa = load_scalar_i32(p.page_table, pt_row + la);
-    int pb = load_scalar_i32(p.page_table, pt_row + lb);
-    pa = pa < 0 ? 0 : (pa >= p.num_pages ? p.num_pages - 1 : pa);
-    pb = pb < 0 ? 0 : (pb >= p.num_pages ? p.num_pages - 1 : pb);
-    const int64_t ea = (int64_t)pa * pstr + h * hstr + (int64_t)(key0 & pmask) * sstr;
-    const int64_t eb = (int64_t)pb * pstr + h * hstr + (int64_t)((key0 + 16) & pmask) * sstr;
-    const char* ka = (const char*)(kbase + ea);
-    const char* kb = (const char*)(kbase + eb);
-    const char* va = (const char*)(vbase + ea);
-    const char* vb2 = (const char*)(vbase + eb);
-#pragma unroll
-    for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int t = rt + RT * i;                  // load instruction index: rows 4t .. 4t+3
-      const uint32_t off = (uint32_t)(4 * (t & 3) + ld_row) * sstr_b + (uint32_t)ld_chunk * 16u;
-      // the prefix K/V is read exactly once: whole lines, non-temporal
-      kd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? kb : ka) + off));
-      vd[i] = __builtin_nontemporal_load((const u32x4*)((t >= 4 ? vb2 : va) + off));
-    }
-  };
   // Stage this wave's share of a block into the LDS tiles; rows at or past
   // `kend` get zero V so masked weights never meet NaN.
   auto stage = [&](int key0, int kend, u32x4 (&kd)[kLoadsPerWave], u32x4 (&vd)[kLoadsPerWave], int buf) {
@@ -356,14 +369,11 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   };
 
   // ---- target blocks: tb = ks + KS * it, software-pipelined PF blocks ahead ----
+  // (the first PF blocks were issued before the query setup)
   // (a wave's share of a block is 8 / RT load instructions, so waves that
   // share their tiles with others keep more blocks in flight)
   {
     const int iters = (nt + KS - 1) / KS;          // same for every wave of the workgroup
-    u32x4 kst[PF][kLoadsPerWave], vst[PF][kLoadsPerWave];
-#pragma unroll
-    for (int u = 0; u < PF; ++u)
-      if (ks + KS * u < nt) issue_target(ks + KS * u, kst[u], vst[u]);
     if constexpr (RT == 1) {
       // private tiles: stage block it from ring slot it % PF, refill the slot
       // with block it + PF, compute (wave-local ordering only)
@@ -499,39 +509,39 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
       }
     }
   }
-  if (ks != 0 || !row_ok) return;
-
   // ---- write: final output (one split) or split partial ----
-  if (p.splits == 1) {
-    const float inv = 1.0f / l_row;
-    const int64_t orow = (((int64_t)b * p.nq + j) * p.hq + hq) * kHeadDim;
+  if (ks == 0 && row_ok) {
+    if (p.splits == 1) {
+      const float inv = 1.0f / l_row;
+      const int64_t orow = (((int64_t)b * p.nq + j) * p.hq + hq) * kHeadDim;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
+      for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = dt * 32 + q4 * 8 + hh * 4;
-        const float o0 = oacc[dt][q4 * 4 + 0] * inv, o1 = oacc[dt][q4 * 4 + 1] * inv;
-        const float o2 = oacc[dt][q4 * 4 + 2] * inv, o3 = oacc[dt][q4 * 4 + 3] * inv;
-        if (p.out_fp32) {
-          *(f32x4*)((float*)p.out + orow + d) = f32x4{o0, o1, o2, o3};
-        } else {
-          *(u32x2*)((uint16_t*)p.out + orow + d) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = dt * 32 + q4 * 8 + hh * 4;
+          const float o0 = oacc[dt][q4 * 4 + 0] * inv, o1 = oacc[dt][q4 * 4 + 1] * inv;
+          const float o2 = oacc[dt][q4 * 4 + 2] * inv, o3 = oacc[dt][q4 * 4 + 3] * inv;
+          if (p.out_fp32) {
+            *(f32x4*)((float*)p.out + orow + d) = f32x4{o0, o1, o2, o3};
+          } else {
+            *(u32x2*)((uint16_t*)p.out + orow + d) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
+          }
         }
       }
+      if (p.lse && hh == 0) p.lse[((int64_t)b * p.nq + j) * p.hq + hq] = (M + __log2f(l_row)) * kLn2;
+    } else {
+      const int64_t prow = (((int64_t)b * p.hkv + h) * p.rows_pad + r) * p.splits + split;
+      float* po = p.part_o + prow * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = dt * 32 + q4 * 8 + hh * 4;
+          *(f32x4*)(po + d) = f32x4{oacc[dt][q4 * 4 + 0], oacc[dt][q4 * 4 + 1], oacc[dt][q4 * 4 + 2],
+                                    oacc[dt][q4 * 4 + 3]};
+        }
+      if (hh == 0) p.part_ml[prow] = make_float2(M, l_row);
     }
-    if (p.lse && hh == 0) p.lse[((int64_t)b * p.nq + j) * p.hq + hq] = (M + __log2f(l_row)) * kLn2;
-  } else {
-    const int64_t prow = (((int64_t)b * p.hkv + h) * p.rows_pad + r) * p.splits + split;
-    float* po = p.part_o + prow * kHeadDim;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = dt * 32 + q4 * 8 + hh * 4;
-        *(f32x4*)(po + d) = f32x4{oacc[dt][q4 * 4 + 0], oacc[dt][q4 * 4 + 1], oacc[dt][q4 * 4 + 2],
-                                  oacc[dt][q4 * 4 + 3]};
-      }
-    if (hh == 0) p.part_ml[prow] = make_float2(M, l_row);
   }
 }
 
@@ -548,20 +558,31 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
 #define KVSHOT_QSPLIT_MAX_RT 1
 #endif
 
-int mfma_waves_per_wg(int row_tiles) { return row_tiles >= 8 ? 8 : 4; }
+int mfma_waves_per_wg(int kernel_row_tiles) { return kernel_row_tiles >= 8 ? 8 : 4; }
 
-// Workgroups of the kernel for `row_tiles` that one CU (4 SIMDs) holds at once.
-int mfma_wgs_per_cu(int row_tiles) {
-  const int wps = row_tiles == 1 ? KVSHOT_RT1_WPS : 2;
-  const int wgs = 4 * wps / mfma_waves_per_wg(row_tiles);
+// Workgroups of the kernel for `kernel_row_tiles` that one CU (4 SIMDs) holds at once.
+int mfma_wgs_per_cu(int kernel_row_tiles) {
+  const int wps = kernel_row_tiles == 1 ? KVSHOT_RT1_WPS : 2;
+  const int wgs = 4 * wps / mfma_waves_per_wg(kernel_row_tiles);
   return wgs < 1 ? 1 : wgs;
 }
 
-hipError_t launch_attn_mfma(const AttnParams& p, int row_tiles, hipStream_t s) {
-  const dim3 grid(p.splits, p.hkv, p.batch);
+// Largest query tile one workgroup holds (in 32-row tiles); taller tiles run
+// as several workgroups per (sequence, KV head, split), each with its own rows
+// and its own copy of the K/V stream (kept on one L2 by the XCD renumbering).
+// One 8-wave workgroup for 256 rows measures faster than two 4-wave ones.
+#ifndef KVSHOT_MAX_KERNEL_ROW_TILES
+#define KVSHOT_MAX_KERNEL_ROW_TILES 8
+#endif
+int mfma_kernel_row_tiles(int row_tiles) {
+  return row_tiles > KVSHOT_MAX_KERNEL_ROW_TILES ? KVSHOT_MAX_KERNEL_ROW_TILES : row_tiles;
+}
+
+hipError_t launch_attn_mfma(const AttnParams& p, int kernel_row_tiles, hipStream_t s) {
+  const dim3 grid((unsigned)((int64_t)p.splits * p.row_groups * p.hkv * p.batch));
   constexpr bool q1 = KVSHOT_QSPLIT_MAX_RT >= 1, q2 = KVSHOT_QSPLIT_MAX_RT >= 2, q4 = KVSHOT_QSPLIT_MAX_RT >= 4,
                  q8 = KVSHOT_QSPLIT_MAX_RT >= 8;
-  switch (row_tiles) {
+  switch (kernel_row_tiles) {
     case 1:
       hipLaunchKernelGGL((attn_mfma_kernel<1, 4, KVSHOT_RT1_PF, q1, KVSHOT_RT1_WPS>), grid, dim3(256), 0, s, p);
       break;

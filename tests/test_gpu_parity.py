@@ -271,3 +271,40 @@ def test_mask_probe_nonzero_pattern_is_the_allowed_set():
                     allowed = list(range(int(c.step_offsets[b]) + i + 1))
                 nz = np.nonzero(out[b, i, 0])[0].tolist()
                 assert nz == allowed, (mode, b, i)
+
+
+def test_hip_graph_replay_matches_eager():
+    """A captured step replays to the eager result, with eager work and syncs between replays."""
+    torch = pytest.importorskip("torch")
+    c = small(ctx_lens=[3000, 700, 0], n_new=8, seed=141)
+    dc = G.DevCase(c)
+    with G.handle_for(c) as att:
+        att.set_option(0, 3)                       # force split-K so the combine kernel is captured too
+        out = torch.empty((3, 8, 32, 128), dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty((3, 8, 32), dtype=torch.float32, device="cuda")
+
+        def step():
+            att.step(dc.q, dc.k_pages, dc.v_pages, dc.page_table, dc.ctx_lens, dc.draft_k, dc.draft_v, dc.extra,
+                     max_ctx=3000, out=out, lse=lse)
+        step()
+        torch.cuda.synchronize()
+        eager, eager_lse = out.clone(), lse.clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for rep in range(4):
+            out.zero_()
+            lse.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, eager), rep
+            assert torch.equal(lse, eager_lse), rep
+            step()                                 # eager work between replays
+            torch.cuda.synchronize()
