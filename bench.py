@@ -358,8 +358,8 @@ def main():
     achieved = attn_launch_bytes / (attn_ms * 1e-3) / 1e9
     traffic = read_traffic(args.workload, args.mode) if not args.splits else None
     path_name = {1: "attn_mfma_kernel", 2: "attn_generic_kernel"}[plan["path"]]
-    kernel = f"{path_name}<{plan['row_tiles']},{8 if plan['row_tiles'] >= 8 else 4}>" if plan["path"] == 1 \
-        else path_name
+    kernel = f"{path_name} ({plan['row_tiles']} x 32-row query tiles per (sequence, KV head))" \
+        if plan["path"] == 1 else path_name
     res = {
         "metric": METRIC,
         "value": round(value, 2),

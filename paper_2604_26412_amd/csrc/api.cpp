@@ -86,7 +86,7 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
     pl.kernel_row_tiles = mfma_kernel_row_tiles(pl.row_tiles);
     pl.row_groups = pl.row_tiles / pl.kernel_row_tiles;
     pl.waves_per_wg = mfma_waves_per_wg(pl.kernel_row_tiles);
-    pl.key_streams = pl.waves_per_wg / pl.kernel_row_tiles;
+    pl.key_streams = mfma_key_streams(pl.kernel_row_tiles);
   }
   const int nb = (max_ctx + kBlockKeys - 1) / kBlockKeys;
   const int pairs = batch * c->cfg.num_kv_heads * pl.row_groups;   // workgroups per split

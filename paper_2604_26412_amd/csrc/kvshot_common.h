@@ -188,5 +188,6 @@ hipError_t launch_validate(const AttnParams& p, int max_ctx_hint, int32_t* flag,
 hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int blocks, hipStream_t s);
 int mfma_waves_per_wg(int row_tiles);
 int mfma_wgs_per_cu(int kernel_row_tiles);
+int mfma_key_streams(int kernel_row_tiles);
 int mfma_kernel_row_tiles(int row_tiles);
 }  // namespace kvshot
