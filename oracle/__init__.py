@@ -31,6 +31,11 @@ Parity status per function:
     above plus step-by-step == folded and page-permutation invariance; the
     softmax scale (1/sqrt(D)) and GQA head mapping are conventions:
     parity unpinned against the paper.
+  * ``fusion.gated_delta_fusion`` -- the hybrid drafter's gated delta rule
+    (Sec. 3.4.1, Eqs. (delta) and (fusion)); pinned (gate shut gives n, gate
+    open with W_Delta = I gives o, block identity of [n; o; Delta], unit
+    Delta selects a column); the cross-only variant (n read as zero) is a
+    reading: parity unpinned.
 """
 from .attention import (  # noqa: F401
     decode,
@@ -44,3 +49,4 @@ from .attention import (  # noqa: F401
     draft_attention,
     gather_dense,
 )
+from .fusion import gated_delta_fusion, sigmoid  # noqa: F401,E402
