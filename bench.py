@@ -214,8 +214,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8"])
+    ap.add_argument("--op", choices=["attention", "fusion"], default="attention",
+                    help="attention: the draft-step attention path (default); fusion: the hybrid drafter's "
+                         "gated delta fusion")
+    ap.add_argument("--workload", default=None,
+                    choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8",
+                             "fusion_t64_d4096", "fusion_t480_d4096"])
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--cold", action="store_true",
@@ -224,6 +228,8 @@ def main():
                     help="launch each step from Python instead of replaying a captured HIP graph of it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=1004)
+    ap.add_argument("--fusion-row-major", action="store_true",
+                    help="--op fusion: read the weights in their row-major layout instead of the packed copy")
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,
                     help="also run one plain device copy of this many GiB (counter calibration under a profiler)")
     args = ap.parse_args()
@@ -238,6 +244,12 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.op == "fusion":
+        return bench_fusion(args, torch, K, W)
+    if args.workload is None:
+        args.workload = DEFAULT_WORKLOAD
+    if args.workload.startswith("fusion"):
+        raise SystemExit("fusion workloads run with --op fusion")
     if args.workload == DEFAULT_WORKLOAD:
         log("generating the 64 x 32768 workload on the device")
         d = make_long_range_on_device(torch, args.seed)
@@ -397,6 +409,192 @@ def main():
         res["parity_sample"] = parity
     print(json.dumps(res), flush=True)
     att.close()
+
+
+# ---------------------------------------------------------------------------
+# gated delta fusion (--op fusion)
+# ---------------------------------------------------------------------------
+
+PEAK_BF16_TFLOPS = 2500.0
+FUSION_METRIC = "gated-delta fusion tokens/s (d=4096, bf16) with achieved TFLOP/s and HBM GB/s"
+
+
+def fusion_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("fusion.hip", "fusion_common.h", "kvshot_common.h"):
+        h.update(open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_fusion_traffic(workload: str):
+    path = os.path.join(PROFILES, f"fusion_kernel_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not (m and f and w) or m.group(1) != fusion_source_hash():
+        return None
+    return float(f.group(1)) + float(w.group(1))
+
+
+def fusion_cpu_baseline(case, h_gpu, budget_s=10.0):
+    """Time the float64 fusion oracle on a bounded sample of the workload's tokens."""
+    import numpy as np
+
+    import oracle
+    import workloads as W
+
+    dec = lambda b: W.bf16_bits_to_f32(b).astype(np.float64)
+    wg, wd, bg = dec(case.w_g), dec(case.w_delta), case.b_g.astype(np.float64)
+    t0 = time.perf_counter()
+    ref = oracle.gated_delta_fusion(dec(case.n[:1]), dec(case.o[:1]), wg, bg, wd)
+    t1 = time.perf_counter() - t0
+    ns = int(max(1, min(case.tokens - 1, 64, budget_s // max(t1, 1e-3))))
+    rows = list(range(1, 1 + ns))
+    t0 = time.perf_counter()
+    ref2 = oracle.gated_delta_fusion(dec(case.n[rows]), dec(case.o[rows]), wg, bg, wd)
+    dt = time.perf_counter() - t0
+    allref = np.concatenate([ref, ref2], 0)
+    got = h_gpu[[0] + rows].float().cpu().numpy().astype(np.float64)
+    diff = got - allref
+    parity = dict(max_abs=float(np.abs(diff).max()), rel_l2=float(np.linalg.norm(diff) / np.linalg.norm(allref)),
+                  tokens=1 + ns)
+    return dict(value=round(ns / dt, 3), unit="tokens/s", cores=blas_threads(), kind="oracle",
+                host_cpus=os.cpu_count(), seconds=round(dt, 3),
+                sample=f"{ns} tokens of the same workload (weights decoded once, outside the timing), float64 "
+                       f"NumPy oracle"), parity
+
+
+def bench_fusion(args, torch, K, W):
+    name = args.workload or "fusion_t64_d4096"
+    if name not in W.FUSION_WORKLOADS:
+        raise SystemExit(f"--op fusion takes one of {sorted(W.FUSION_WORKLOADS)}")
+    spec = W.FUSION_WORKLOADS[name]
+    log(f"generating {name} on the host")
+    case = W.fusion_case(spec["tokens"], spec["d"], seed=spec["seed"])
+    tokens, d = case.tokens, case.d
+
+    def dev(a):
+        import numpy as np
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    n, o, w_g, b_g, w_delta = dev(case.n), dev(case.o), dev(case.w_g), dev(case.b_g), dev(case.w_delta)
+    h = torch.empty((tokens, d), dtype=torch.bfloat16, device="cuda")
+    fz = K.GatedDeltaFusion(d, tokens)
+    if args.splits:
+        fz.set_option(K.OPT_SPLITS, args.splits)
+    plan = fz.plan(tokens)
+    # weights are packed once, as a serving engine does at load time (outside the timed region)
+    packed = None if args.fusion_row_major else fz.pack_weights(w_g, w_delta)
+    torch.cuda.synchronize()
+
+    def step():
+        if packed is None:
+            fz(n, o, w_g, b_g, w_delta, out=h)
+        else:
+            fz(n, o, None, b_g, None, out=h, packed=packed)
+
+    if args.copy_calib_gib > 0:
+        nbytes = int(args.copy_calib_gib * (1 << 30))
+        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
+        del src, dst
+
+    log(f"plan {plan}; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    run_step = step
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        for _ in range(args.warmup):
+            run_step()
+        torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    fz.set_option(K.OPT_PROFILE, 1)
+    for _ in range(args.steps):
+        step()
+    prof = fz.profile_read()
+    fz.set_option(K.OPT_PROFILE, 0)
+    calls = max(1, prof["calls"])
+    main_ms, comb_ms = prof["main_ms"] / calls, prof["combine_ms"] / calls
+    log(f"step {ms_per_step:.4f} ms; fusion kernel {main_ms:.4f} ms; combine {comb_ms:.4f} ms")
+
+    alg = W.fusion_algorithmic(tokens, d)
+    out_bytes = tokens * d * 2
+    part_bytes = plan["splits"] * tokens * d * 8 if plan["splits"] > 1 else 0
+    # main kernel: weights, bias and activations in; the output (one split) or the split partials out
+    main_bytes = alg["bytes"] - out_bytes + (part_bytes if part_bytes else out_bytes)
+    intensity = alg["flops"] / alg["bytes"]
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if intensity >= ridge:
+        roof = {"bound": "mfma", "achieved": round(alg["flops"] / (main_ms * 1e-3) / 1e12, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(main_bytes / (main_ms * 1e-3) / 1e9, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = read_fusion_traffic(name) if not args.splits else None
+    roof.update({"kernel": f"fusion_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)",
+                 "kernel_ms": round(main_ms, 5), "combine_ms": round(comb_ms, 5),
+                 "algorithmic_bytes_per_launch": main_bytes, "flops_per_launch": alg["flops"],
+                 "arithmetic_intensity_flop_per_byte": round(intensity, 1),
+                 "achieved_tflops": round(alg["flops"] / (main_ms * 1e-3) / 1e12, 2),
+                 "achieved_gbs": round(main_bytes / (main_ms * 1e-3) / 1e9, 2)})
+    res = {
+        "metric": FUSION_METRIC,
+        "value": round(tokens / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {tokens} tokens, d {d}, W_g {d}x{3 * d}, W_Delta {d}x{d}, bf16",
+                   "tokens": tokens, "d": d, "splits": plan["splits"], "workgroups": plan["workgroups"],
+                   "weights": "row-major" if packed is None else "packed once before timing",
+                   "launch": "python" if args.no_graph else "hip graph replay"},
+        "roofline": roof,
+        "step_tflops": round(alg["flops"] / (ms_per_step * 1e-3) / 1e12, 2),
+        "step_hbm_gbs": round(alg["bytes"] / (ms_per_step * 1e-3) / 1e9, 2),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cb, parity = fusion_cpu_baseline(case, h)
+        res["cpu_baseline"] = cb
+        res["parity_sample"] = parity
+    print(json.dumps(res), flush=True)
+    fz.close()
 
 
 if __name__ == "__main__":

@@ -13,7 +13,7 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["DraftAttention", "KvshotError", "load_library", "LIB_PATH", "EXPORTED_SYMBOLS"]
+__all__ = ["DraftAttention", "GatedDeltaFusion", "KvshotError", "load_library", "LIB_PATH", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
@@ -28,7 +28,11 @@ EXPORTED_SYMBOLS = [
     "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
     "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_debug_stream_read",
     "kvshot_status_string",
+    "kvshot_fusion_init", "kvshot_fusion_destroy", "kvshot_gated_delta_fusion", "kvshot_fusion_set_option",
+    "kvshot_fusion_plan", "kvshot_fusion_profile_read", "kvshot_fusion_pack_weights",
+    "kvshot_gated_delta_fusion_packed",
 ]
+FUSION_CROSS_ONLY, FUSION_OUT_FP32 = 1, 2
 
 
 class KvshotConfig(ctypes.Structure):
@@ -76,6 +80,15 @@ def load_library(path: Optional[str] = None):
         "kvshot_debug_gather_kv": [_vp, _i32, _i32] + [_vp] * 7,
         "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
         "kvshot_debug_stream_read": [_vp, _i64, _vp, _i32, _vp],
+        "kvshot_fusion_init": [_i32, _i32, ctypes.POINTER(_vp)],
+        "kvshot_fusion_destroy": [_vp],
+        "kvshot_gated_delta_fusion": [_vp, _i32] + [_vp] * 7 + [_i32, _vp],
+        "kvshot_fusion_set_option": [_vp, _i32, _i64],
+        "kvshot_fusion_pack_weights": [_vp, _vp, _vp, _vp, _vp],
+        "kvshot_gated_delta_fusion_packed": [_vp, _i32] + [_vp] * 6 + [_i32, _vp],
+        "kvshot_fusion_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32)],
+        "kvshot_fusion_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(_i64)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -295,3 +308,106 @@ class DraftAttention:
             self._h, B, n, self._tensor(parents, "parents", torch.int32, (B, n)), anc.data_ptr(), depth.data_ptr(),
             self._stream(stream)))
         return anc, depth
+
+
+class GatedDeltaFusion:
+    """Handle for the hybrid drafter's gated delta fusion (C ABI in ``include/kvshot_fusion.h``).
+
+    ``h = n + sigmoid(W_g [n; o; o - n] + b_g) * (W_Delta (o - n))`` per token,
+    with bf16 activations and weights and a float32 bias.
+    """
+
+    def __init__(self, d: int, max_tokens: int):
+        self._lib = load_library()
+        self.d, self.max_tokens = int(d), int(max_tokens)
+        h = _vp()
+        _check("kvshot_fusion_init", self._lib.kvshot_fusion_init(self.d, self.max_tokens, ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            self._lib.kvshot_fusion_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    @staticmethod
+    def _tensor(t, name, dtype, shape):
+        torch = _torch()
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
+        if t.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        return t.data_ptr()
+
+    def __call__(self, n, o, w_g, b_g, w_delta, *, out=None, gate=None, cross_only=False, out_dtype="bf16",
+                 packed=None, stream=None):
+        """Returns ``out`` [tokens][d]; ``gate`` (float32 [tokens][d]) is filled when given.
+
+        With ``packed`` (from :meth:`pack_weights`), ``w_g`` and ``w_delta`` are not read and may be None.
+        """
+        torch = _torch()
+        bf = torch.bfloat16
+        tokens, d = o.shape[0], self.d
+        od = torch.bfloat16 if out_dtype in ("bf16", "bfloat16") else torch.float32
+        if out is None:
+            out = torch.empty((tokens, d), dtype=od, device=o.device)
+        n_ptr = None if (cross_only and n is None) else self._tensor(n, "n", bf, (tokens, d))
+        flags = (FUSION_CROSS_ONLY if cross_only else 0) | (FUSION_OUT_FP32 if od == torch.float32 else 0)
+        o_ptr = self._tensor(o, "o", bf, (tokens, d))
+        b_ptr = self._tensor(b_g, "b_g", torch.float32, (d,))
+        out_ptr = self._tensor(out, "out", od, (tokens, d))
+        g_ptr = self._tensor(gate, "gate", torch.float32, (tokens, d)) if gate is not None else None
+        s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+        if packed is not None:
+            _check("kvshot_gated_delta_fusion_packed", self._lib.kvshot_gated_delta_fusion_packed(
+                self._h, tokens, n_ptr, o_ptr, self._tensor(packed, "packed", bf, (4 * d * d,)), b_ptr, out_ptr,
+                g_ptr, flags, s))
+        else:
+            _check("kvshot_gated_delta_fusion", self._lib.kvshot_gated_delta_fusion(
+                self._h, tokens, n_ptr, o_ptr, self._tensor(w_g, "w_g", bf, (d, 3 * d)), b_ptr,
+                self._tensor(w_delta, "w_delta", bf, (d, d)), out_ptr, g_ptr, flags, s))
+        return out
+
+    def pack_weights(self, w_g, w_delta, packed=None, stream=None):
+        """Packed copy of both weight matrices (bf16 [4 d^2]) for ``__call__(..., packed=...)``."""
+        torch = _torch()
+        d = self.d
+        if packed is None:
+            packed = torch.empty((4 * d * d,), dtype=torch.bfloat16, device=w_g.device)
+        _check("kvshot_fusion_pack_weights", self._lib.kvshot_fusion_pack_weights(
+            self._h, self._tensor(w_g, "w_g", torch.bfloat16, (d, 3 * d)),
+            self._tensor(w_delta, "w_delta", torch.bfloat16, (d, d)),
+            self._tensor(packed, "packed", torch.bfloat16, (4 * d * d,)),
+            stream if stream is not None else torch.cuda.current_stream().cuda_stream))
+        return packed
+
+    def set_option(self, option: int, value: int):
+        _check("kvshot_fusion_set_option", self._lib.kvshot_fusion_set_option(self._h, option, value))
+
+    def plan(self, tokens: int):
+        s, w = _i32(0), _i32(0)
+        _check("kvshot_fusion_plan", self._lib.kvshot_fusion_plan(self._h, tokens, ctypes.byref(s), ctypes.byref(w)))
+        return dict(splits=s.value, workgroups=w.value)
+
+    def profile_read(self):
+        a, c, k = ctypes.c_double(0), ctypes.c_double(0), _i64(0)
+        _check("kvshot_fusion_profile_read", self._lib.kvshot_fusion_profile_read(
+            self._h, ctypes.byref(a), ctypes.byref(c), ctypes.byref(k)))
+        return dict(main_ms=a.value, combine_ms=c.value, calls=k.value)

@@ -1,0 +1,376 @@
+// Gated delta fusion of the hybrid drafter on bf16 MFMA (gfx950).
+//
+// Sec. 3.4.1, Eqs. (delta) and (fusion), shapes from App. B ("Shared gate"):
+// for each draft token, Delta = o - n, g = sigmoid(W_g [n; o; Delta] + b_g)
+// and h = n + g * (W_Delta Delta).  The gate and the delta projection land on
+// the same output element, so one workgroup computes both for a tile of 64
+// tokens x 128 channels and applies the epilogue in registers.
+//
+// Reduction space: four segments of length d -- (n, W_g[:, 0:d]),
+// (o, W_g[:, d:2d]) and (Delta, W_g[:, 2d:3d]) into the gate accumulator,
+// (Delta, W_Delta) into the delta accumulator.  With few tokens (one draft
+// step of a batch) the segments, and then halves of them, are split over
+// workgroups so the grid still fills the chip; a second kernel sums the
+// split partials and applies the epilogue.
+//
+// Operands: activations are the A operand (rows = tokens).  They are staged
+// through LDS, where Delta is formed once per element (o - n in float32,
+// rounded to bf16).  Weights are the B operand (columns = channels), loaded
+// straight into registers.  Within a chunk of kKC reduction indices, a lane of
+// half h covers indices h kKC/2 .. (h + 1) kKC/2 - 1, and MFMA k-step s takes
+// indices h kKC/2 + 8s .. + 7 from both operands (any pairing of operand
+// slots with reduction indices gives the same sum, as long as A and B agree).
+//
+// Weight layouts: the row-major matrices as given (a lane's 16-byte loads
+// are kKC contiguous bytes of one weight row, so one load instruction touches
+// 32 rows), or a packed copy made once by fusion_pack_kernel in which the
+// 16-byte pieces sit in exactly the order the waves load them:
+//   [channel tile][segment][chunk][wave][k-step s][lane][8 values],
+// so every load instruction reads 1 KB contiguous and one workgroup's chunk of
+// a segment is contiguous.
+#include "fusion_common.h"
+
+namespace kvshot {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#ifndef KVSHOT_FUSION_STAGE_FIRST
+#define KVSHOT_FUSION_STAGE_FIRST 1
+#endif
+#ifndef KVSHOT_FUSION_KC
+#define KVSHOT_FUSION_KC 64
+#endif
+constexpr int kKC = KVSHOT_FUSION_KC;                  // reduction chunk per loop iteration (d % (2 kKC) == 0)
+constexpr int kSteps = kKC / 16;                       // MFMA k-steps per chunk
+constexpr int kHalfSpan = kKC / 2;                     // reduction indices per lane half and chunk
+constexpr int kPitch = kKC + 8;                        // LDS row pitch (bf16): rows shift by 4 banks, so 16-byte row reads are conflict-free
+constexpr int kRowPieces = kKC / 8;                    // 16-byte pieces per activation row and chunk
+constexpr int kAPieces = kFusionTokens * kRowPieces / 256;   // pieces per thread and tensor
+constexpr int kTileElems = kFusionTokens * kPitch;     // one activation tile
+static_assert(kKC == 64 || kKC == 128, "chunk size");
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// o - n per bf16 element (exact in float32), rounded to bf16
+__device__ __forceinline__ u32x4 bf16x8_sub(u32x4 o, u32x4 n) {
+  u32x4 r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = pack_bf16x2(bf16_lo(o[e]) - bf16_lo(n[e]), bf16_hi(o[e]) - bf16_hi(n[e]));
+  return r;
+}
+
+__device__ __forceinline__ float sigmoidf_fast(float z) {
+  // 1 / (1 + 2^(-z log2 e)); saturates to exactly 0 and 1 for large |z|
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-z * 1.4426950408889634f));
+}
+
+// NSEG: segments of the reduction space this workgroup covers (4: all of
+// them; 2 or 1 when split).  Segment i of a split is seg0 + i.  PF: chunks in
+// flight (activation and weight registers of each).
+// WPS: workgroups per CU the register budget allows (a split kernel with one
+// segment is small enough for two, which hides each one's per-chunk latency).
+template <int NSEG, int PF, bool PACKED, int WPS>
+__global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
+  static_assert(PF >= 2, "activations are staged one chunk ahead of the slot being computed");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][3][kTileElems];   // [buffer][n, o, Delta]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hh = lane >> 5;
+  // work item: (channel tile, split) major, token tile minor -- workgroups that
+  // read the same weights are numbered together and so share one XCD's L2
+  int wi = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = wi % p.m_tiles;
+  wi /= p.m_tiles;
+  const int split = wi % p.splits;
+  const int ntile = wi / p.splits;
+  const int m0 = mt * kFusionTokens;
+  const int d = p.d;
+  const int kparts = p.splits > 4 ? p.splits / 4 : 1;   // reduction-index parts per segment
+  const int seg0 = NSEG == 4 ? 0 : (split / kparts) * NSEG;
+  const int klen = d / kparts;
+  const int kbeg = (split % kparts) * klen;
+  const int nchunks = klen / kKC;
+
+  const bool cross_only = p.cross_only != 0;
+  const bool has_n = seg0 == 0 && !cross_only;          // segment 0 reads n (zero when cross-only)
+  const bool has_o = seg0 <= 1 && seg0 + NSEG > 1;      // segment 1 reads o
+  const bool has_delta = seg0 + NSEG > 2;               // segments 2 and 3 read Delta
+  const bool load_n = !cross_only && (has_n || has_delta);
+  const bool load_o = has_o || has_delta;
+  // loads are issued unconditionally (from o when n is absent) and masked by select, so the loop has no branches
+  const uint16_t* nsrc = cross_only ? p.o : p.n;
+
+  // ---- activations: thread t stages 16-byte pieces t and t + 256 of each tile ----
+  auto load_a = [&](int chunk, u32x4 (&an)[kAPieces], u32x4 (&ao)[kAPieces]) {
+    const int k0 = kbeg + chunk * kKC;
+#pragma unroll
+    for (int i = 0; i < kAPieces; ++i) {
+      const int pc = tid + 256 * i;
+      int m = m0 + pc / kRowPieces;
+      m = m < p.tokens ? m : p.tokens - 1;
+      const int64_t off = (int64_t)m * d + k0 + 8 * (pc % kRowPieces);
+      const u32x4 vn = *(const u32x4*)(nsrc + (load_n ? off : 0));    // an unneeded tile reads one line
+      const u32x4 vo = *(const u32x4*)(p.o + (load_o ? off : 0));
+      an[i] = load_n ? vn : u32x4{0u, 0u, 0u, 0u};
+      ao[i] = load_o ? vo : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stage_a = [&](int buf, const u32x4 (&an)[kAPieces], const u32x4 (&ao)[kAPieces]) {
+#pragma unroll
+    for (int i = 0; i < kAPieces; ++i) {
+      const int pc = tid + 256 * i;
+      const int row = pc / kRowPieces;
+      const bool valid = m0 + row < p.tokens;           // rows past the last token stay zero
+      const u32x4 vn = valid ? an[i] : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vo = valid ? ao[i] : u32x4{0u, 0u, 0u, 0u};
+      uint16_t* dst = &lds[buf][0][row * kPitch + 8 * (pc % kRowPieces)];
+      *(u32x4*)dst = vn;
+      *(u32x4*)(dst + kTileElems) = vo;
+      *(u32x4*)(dst + 2 * kTileElems) = bf16x8_sub(vo, vn);
+    }
+  };
+
+  // ---- weights: this lane's output channel and the weight row of each segment ----
+  const int wc = ntile * kFusionChannels + w * 32 + (lane & 31);
+  const uint16_t* wrow[NSEG];
+#pragma unroll
+  for (int i = 0; i < NSEG; ++i) {
+    const int seg = seg0 + i;
+    wrow[i] = seg < 3 ? p.w_g + (int64_t)wc * 3 * d + (int64_t)seg * d : p.w_delta + (int64_t)wc * d;
+  }
+  // packed layout: piece (channel tile, segment, chunk, wave, s, lane) at
+  // ((((ntile * 4 + seg) * chunks_per_segment + chunk) * 4 + w) * kSteps + s) * 512 + lane * 8
+  const int chunks_per_segment = d / kKC;
+  const uint16_t* wpk[NSEG];
+#pragma unroll
+  for (int i = 0; i < NSEG; ++i)
+    wpk[i] = p.w_packed + ((((int64_t)ntile * 4 + seg0 + i) * chunks_per_segment + kbeg / kKC) * 4 + w) * kSteps * 512 +
+             lane * 8;
+  auto load_w = [&](int chunk, u32x4 (&dst)[NSEG][kSteps]) {
+    if constexpr (PACKED) {
+#pragma unroll
+      for (int i = 0; i < NSEG; ++i)
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s)
+          dst[i][s] = *(const u32x4*)(wpk[i] + (int64_t)chunk * (4 * kSteps * 512) + s * 512);
+    } else {
+      const int k = kbeg + chunk * kKC + kHalfSpan * hh;
+#pragma unroll
+      for (int i = 0; i < NSEG; ++i)
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) dst[i][s] = *(const u32x4*)(wrow[i] + k + 8 * s);
+    }
+  };
+
+  // Accumulators: with all four segments, [0] gate and [1] delta projection;
+  // with a split, one per segment of the split.  Segment seg reads activation
+  // tile min(seg, 2) (n, o, Delta) -- an address, not a branch.
+  constexpr int NACC = NSEG == 4 ? 2 : NSEG;
+  f32x16 acc[NACC][2];
+#pragma unroll
+  for (int a = 0; a < NACC; ++a) acc[a][0] = acc[a][1] = f32x16{};
+  int tile_of[NSEG];
+#pragma unroll
+  for (int i = 0; i < NSEG; ++i) tile_of[i] = min(seg0 + i, 2) * kTileElems;
+
+  auto compute = [&](int buf, const u32x4 (&wr)[NSEG][kSteps]) {
+    const uint16_t* base = &lds[buf][0][0];
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh + 8 * s;
+        if constexpr (NSEG == 4) {
+          const bf16x8 a_n = as_bf16x8(*(const u32x4*)(base + off));
+          const bf16x8 a_o = as_bf16x8(*(const u32x4*)(base + kTileElems + off));
+          const bf16x8 a_d = as_bf16x8(*(const u32x4*)(base + 2 * kTileElems + off));
+          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_n, as_bf16x8(wr[0][s]), acc[0][t], 0, 0, 0);
+          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_o, as_bf16x8(wr[1][s]), acc[0][t], 0, 0, 0);
+          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_d, as_bf16x8(wr[2][s]), acc[0][t], 0, 0, 0);
+          acc[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_d, as_bf16x8(wr[3][s]), acc[1][t], 0, 0, 0);
+        } else {
+#pragma unroll
+          for (int i = 0; i < NSEG; ++i) {
+            const bf16x8 a = as_bf16x8(*(const u32x4*)(base + tile_of[i] + off));
+            acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(wr[i][s]), acc[i][t], 0, 0, 0);
+          }
+        }
+      }
+    }
+  };
+
+  // ---- main loop ----
+  // Ring slot c % PF holds the activation and weight registers of chunk c.
+  // Chunk c is computed from LDS buffer c & 1 and its weight slot; then the
+  // activations of chunk c + 1 go to the other buffer, and the slot is
+  // refilled with chunk c + PF.  Every refill is issued (clamped to the last
+  // chunk; iterations past the last chunk only keep the pattern), so the
+  // loads behind each slot are the same on every path and the waits cover
+  // just the slot in use.
+  u32x4 ran[PF][kAPieces], rao[PF][kAPieces];
+  u32x4 wreg[PF][NSEG][kSteps];
+  const int last = nchunks - 1;
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    load_a(min(u, last), ran[u], rao[u]);
+    load_w(min(u, last), wreg[u]);
+  }
+  stage_a(0, ran[0], rao[0]);
+  __syncthreads();
+  for (int c0 = 0; c0 < nchunks; c0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int c = c0 + u;
+#if KVSHOT_FUSION_STAGE_FIRST
+      // the other buffer's activations first: their LDS writes overlap this chunk's products
+      if (c + 1 < nchunks) stage_a((c + 1) & 1, ran[(u + 1) % PF], rao[(u + 1) % PF]);
+      if (c < nchunks) compute(c & 1, wreg[u]);
+#else
+      if (c < nchunks) compute(c & 1, wreg[u]);
+      if (c + 1 < nchunks) stage_a((c + 1) & 1, ran[(u + 1) % PF], rao[(u + 1) % PF]);
+#endif
+      load_a(min(c + PF, last), ran[u], rao[u]);
+      load_w(min(c + PF, last), wreg[u]);
+      __syncthreads();
+    }
+  }
+
+  // ---- epilogue: accumulator register v of lane (channel, hh) is token 8(v/4) + 4hh + v%4 of its 32-row tile ----
+  const bool fused = p.splits == 1;
+  const float bias = fused ? p.b_g[wc] : 0.0f;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
+      if (m >= p.tokens) continue;
+      const int64_t idx = (int64_t)m * d + wc;
+      // this workgroup's share of the gate pre-activation and of the delta projection
+      float zg = 0.0f, zd = 0.0f;
+      if constexpr (NSEG == 4) {
+        zg = acc[0][t][v];
+        zd = acc[1][t][v];
+      } else {
+#pragma unroll
+        for (int i = 0; i < NSEG; ++i) {
+          if (seg0 + i < 3) zg += acc[i][t][v];
+          else zd += acc[i][t][v];
+        }
+      }
+      if (fused) {
+        const float g = sigmoidf_fast(zg + bias);
+        const float nv = cross_only ? 0.0f : __uint_as_float((uint32_t)p.n[idx] << 16);
+        const float hv = nv + g * zd;
+        if (p.out_fp32) ((float*)p.h)[idx] = hv;
+        else ((uint16_t*)p.h)[idx] = (uint16_t)(pack_bf16x2(hv, 0.0f) & 0xffffu);
+        if (p.g_out) p.g_out[idx] = g;
+      } else {
+        const int64_t plane = (int64_t)p.tokens * d;
+        if (seg0 < 3) p.part[(2 * split) * plane + idx] = zg;
+        if (seg0 + NSEG > 3) p.part[(2 * split + 1) * plane + idx] = zd;
+      }
+    }
+  }
+}
+
+// Split partials -> epilogue: sums, in split order (deterministic), the gate
+// planes and the delta-projection planes that the splits wrote, then
+// h = n + sigmoid(gate + b_g) * delta projection.  One thread per four channels.
+__global__ __launch_bounds__(256) void fusion_combine_kernel(FusionParams p) {
+  const int64_t quads = (int64_t)p.tokens * p.d / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= quads) return;
+  const int64_t idx = 4 * i;                            // element (m, c), c % 4 == 0
+  const int c = (int)(idx % p.d);
+  const int64_t plane = (int64_t)p.tokens * p.d;
+  f32x4 g = {0.f, 0.f, 0.f, 0.f}, e = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < p.splits; ++s) {
+    if ((p.part_g_mask >> s) & 1u) g += *(const f32x4*)(p.part + (2 * s) * plane + idx);
+    if ((p.part_d_mask >> s) & 1u) e += *(const f32x4*)(p.part + (2 * s + 1) * plane + idx);
+  }
+  const f32x4 b = *(const f32x4*)(p.b_g + c);
+  f32x4 nv = {0.f, 0.f, 0.f, 0.f};
+  if (!p.cross_only) {
+    const uint2 nn = *(const uint2*)(p.n + idx);
+    nv = f32x4{bf16_lo(nn.x), bf16_hi(nn.x), bf16_lo(nn.y), bf16_hi(nn.y)};
+  }
+  f32x4 ga, hv;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    ga[j] = sigmoidf_fast(g[j] + b[j]);
+    hv[j] = nv[j] + ga[j] * e[j];
+  }
+  if (p.out_fp32) *(f32x4*)((float*)p.h + idx) = hv;
+  else *(uint2*)((uint16_t*)p.h + idx) = make_uint2(pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3]));
+  if (p.g_out) *(f32x4*)(p.g_out + idx) = ga;
+}
+
+#ifndef KVSHOT_FUSION_PF4
+#define KVSHOT_FUSION_PF4 2
+#endif
+#ifndef KVSHOT_FUSION_PF2
+#define KVSHOT_FUSION_PF2 3
+#endif
+#ifndef KVSHOT_FUSION_PF1
+#define KVSHOT_FUSION_PF1 4
+#endif
+
+template <bool PACKED>
+void launch_fusion_t(const FusionParams& p, hipStream_t s) {
+  const dim3 grid((unsigned)((int64_t)p.m_tiles * p.n_tiles * p.splits));
+  if (p.splits <= 1) hipLaunchKernelGGL((fusion_kernel<4, KVSHOT_FUSION_PF4, PACKED, 1>), grid, dim3(256), 0, s, p);
+  else if (p.splits == 2)
+    hipLaunchKernelGGL((fusion_kernel<2, KVSHOT_FUSION_PF2, PACKED, 1>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((fusion_kernel<1, KVSHOT_FUSION_PF1, PACKED, 2>), grid, dim3(256), 0, s, p);
+}
+
+// One thread per 16-byte piece of the packed copy: it reads the 8 weights of
+// that piece from the row-major matrices (see the layout above).
+__global__ __launch_bounds__(256) void fusion_pack_kernel(const uint16_t* w_g, const uint16_t* w_delta,
+                                                           uint16_t* packed, int d) {
+  const int64_t pieces = (int64_t)d * d / 2;             // 4 d^2 values / 8 per piece
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= pieces) return;
+  const int cps = d / kKC;
+  const int lane = (int)(q & 63);
+  const int s = (int)((q >> 6) % kSteps);
+  const int w = (int)((q / (64 * kSteps)) & 3);
+  int64_t r = q / (256 * kSteps);
+  const int chunk = (int)(r % cps);
+  r /= cps;
+  const int seg = (int)(r & 3);
+  const int ntile = (int)(r >> 2);
+  const int c = ntile * kFusionChannels + w * 32 + (lane & 31);
+  const int k = chunk * kKC + kHalfSpan * (lane >> 5) + 8 * s;
+  const uint16_t* src = seg < 3 ? w_g + (int64_t)c * 3 * d + (int64_t)seg * d + k : w_delta + (int64_t)c * d + k;
+  *(u32x4*)(packed + q * 8) = *(const u32x4*)src;
+}
+
+}  // namespace
+
+hipError_t launch_fusion(const FusionParams& p, hipStream_t s) {
+  if (p.w_packed) launch_fusion_t<true>(p, s);
+  else launch_fusion_t<false>(p, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fusion_pack(const uint16_t* w_g, const uint16_t* w_delta, uint16_t* packed, int d, hipStream_t s) {
+  const int64_t pieces = (int64_t)d * d / 2;
+  hipLaunchKernelGGL(fusion_pack_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, w_g, w_delta,
+                     packed, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_fusion_combine(const FusionParams& p, hipStream_t s) {
+  const int64_t quads = (int64_t)p.tokens * p.d / 4;
+  hipLaunchKernelGGL(fusion_combine_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace kvshot

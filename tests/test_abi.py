@@ -122,3 +122,17 @@ def test_binding_argument_counts_match_header(lib):
         assert m, name
         params = [p for p in m.group(1).split(",") if p.strip() and p.strip() != "void"]
         assert len(getattr(lib, name).argtypes) == len(params), name
+
+
+@pytest.mark.parametrize("d,max_tokens", [(0, 8), (100, 8), (384, 8), (256, 0), (-256, 8)])
+def test_fusion_init_rejects_bad_sizes_before_any_device_call(lib, d, max_tokens):
+    h = ctypes.c_void_p(123)
+    assert lib.kvshot_fusion_init(d, max_tokens, ctypes.byref(h)) == 1
+    assert h.value is None
+
+
+def test_fusion_null_handle(lib):
+    assert lib.kvshot_gated_delta_fusion(None, 1, None, None, None, None, None, None, None, 0, None) == 1
+    assert lib.kvshot_fusion_set_option(None, 0, 0) == 1
+    assert lib.kvshot_fusion_plan(None, 1, None, None) == 1
+    assert lib.kvshot_fusion_destroy(None) == 0

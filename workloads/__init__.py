@@ -302,3 +302,52 @@ def algorithmic_bytes(case_or_dims, *, elem_bytes: int = 2) -> int:
         tot += 2 * c.draft_len(b) * Hkv * D * elem_bytes
     tot += 2 * c.batch * c.n_new * Hq * D * elem_bytes  # q in, out
     return tot
+
+
+# ---------------------------------------------------------------------------
+# gated delta fusion inputs (the hybrid drafter's fusion step, Sec. 3.4.1):
+# self- and cross-attention outputs of one drafter layer and the fusion's
+# weights, in the linear-layer storage of App. B's shapes.
+# ---------------------------------------------------------------------------
+
+_TID_FN, _TID_FO, _TID_FWG, _TID_FB, _TID_FWD = 4001, 4002, 4003, 4004, 4005
+
+
+@dataclass
+class FusionCase:
+    """Inputs of one fusion call: bf16 bits for activations and weights, float32 bias."""
+    tokens: int
+    d: int
+    n: np.ndarray         # uint16 [tokens][d]
+    o: np.ndarray         # uint16 [tokens][d]
+    w_g: np.ndarray       # uint16 [d][3d]
+    b_g: np.ndarray       # float32 [d]
+    w_delta: np.ndarray   # uint16 [d][d]
+
+
+def fusion_case(tokens: int, d: int, seed: int = 2001, gate_bias_mean: float = -2.0) -> FusionCase:
+    """Seeded fusion inputs: n, o ~ N(0, 1); W_g ~ N(0, 1/(3d)); W_Delta ~ N(0, 1/d);
+    b_g ~ N(gate_bias_mean, 1) (a mostly shut gate, as trained gates settle low)."""
+    n = f32_to_bf16_bits(_normal(seed, _TID_FN, (tokens, d)))
+    o = f32_to_bf16_bits(_normal(seed, _TID_FO, (tokens, d)))
+    w_g = f32_to_bf16_bits(_normal(seed, _TID_FWG, (d, 3 * d)) / np.float32(np.sqrt(3.0 * d)))
+    b_g = (_normal(seed, _TID_FB, (d,)) + np.float32(gate_bias_mean)).astype(np.float32)
+    w_delta = f32_to_bf16_bits(_normal(seed, _TID_FWD, (d, d)) / np.float32(np.sqrt(float(d))))
+    return FusionCase(tokens=tokens, d=d, n=n, o=o, w_g=w_g, b_g=b_g, w_delta=w_delta)
+
+
+# Fusion workloads: d = 4096 is the Qwen3-8B hidden size the drafter shares.
+FUSION_WORKLOADS = {
+    # one draft step of a 64-sequence batch: 64 tokens
+    "fusion_t64_d4096": dict(tokens=64, d=4096, seed=2001),
+    # every node of eight 60-node draft trees in one call: 480 tokens
+    "fusion_t480_d4096": dict(tokens=480, d=4096, seed=2002),
+}
+
+
+def fusion_algorithmic(tokens: int, d: int) -> dict:
+    """Unique bytes (bf16 activations and weights, float32 bias, bf16 output) and flops of one call."""
+    weights = (3 * d * d + d * d) * 2 + d * 4
+    acts = 2 * tokens * d * 2 + tokens * d * 2
+    flops = 2 * tokens * d * (3 * d) + 2 * tokens * d * d
+    return dict(bytes=weights + acts, flops=flops)
