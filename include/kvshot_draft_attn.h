@@ -122,6 +122,62 @@ kvshot_status kvshot_draft_attn_tree(kvshot_handle h, int32_t batch, int32_t n_n
                                      const void* draft_k, const void* draft_v, const int32_t* parents,
                                      void* out, float* lse, void* stream);
 
+/* General form of a call (step or tree), with two additions:
+ *
+ *   pos_base     nullable int32 [batch]: position of draft step 0 (step mode)
+ *                or of depth 0 (tree mode) for sequence b.  NULL means
+ *                ctx_lens[b], as in kvshot_draft_attn_step / _tree.  A separate
+ *                base lets the prefix hold keys that are not one position per
+ *                slot: the KV of L_s sampled target layers concatenated along
+ *                the sequence (the head-concatenation injection of Sec. 3.2,
+ *                read as one softmax over the L_s x T keys), while the draft
+ *                tokens keep positions T + step.  Values are clamped to
+ *                [0, max_position], positions to the RoPE table.
+ *   query_nodes  tree mode, nullable int32 [batch][n_queries]: the tree node
+ *                whose query fills query row j.  The draft keys are always all
+ *                n_nodes nodes, so only the newest level's nodes need queries
+ *                when a tree grows level by level (Sec. 3.5, tree (8, 10, 60)).
+ *                NULL means row j is node j (then n_queries == n_nodes).  Values
+ *                are clamped to [0, n_nodes).
+ *
+ * Step mode: n_nodes is ignored; query j sits at pos_base + s0 + j and sees
+ * draft keys s <= s0 + j, each at pos_base + s.  Tree mode: query row j (node
+ * i = query_nodes[b][j]) sits at pos_base + depth(i) and sees the draft keys
+ * of i and its ancestors, key s at pos_base + depth(s).
+ * Requirements as for kvshot_draft_attn_step / _tree, with G * n_queries <= 256,
+ * 1 <= n_queries <= max_draft and, in tree mode, 1 <= n_nodes <= max_draft. */
+enum { KVSHOT_MODE_STEP = 0, KVSHOT_MODE_TREE = 1 };
+typedef struct kvshot_call {
+  int32_t mode;                 /* KVSHOT_MODE_STEP or KVSHOT_MODE_TREE */
+  int32_t batch;
+  int32_t n_queries;            /* query rows per sequence */
+  int32_t n_nodes;              /* tree mode: nodes (draft keys) per sequence */
+  int32_t max_ctx_len_hint;     /* bounds ctx_lens, sizes the split-K grid */
+  int32_t reserved;             /* must be 0 */
+  const void* q;                /* [batch][n_queries][Hq][D] */
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* page_table;
+  const int32_t* ctx_lens;
+  const void* draft_k;          /* [batch][max_draft][Hkv][D] */
+  const void* draft_v;
+  const int32_t* step_offsets;  /* step mode: [batch] */
+  const int32_t* parents;       /* tree mode: [batch][n_nodes] */
+  const int32_t* query_nodes;   /* tree mode, nullable: [batch][n_queries] */
+  const int32_t* pos_base;      /* nullable: [batch] */
+  void* out;                    /* [batch][n_queries][Hq][D] */
+  float* lse;                   /* nullable: [batch][n_queries][Hq] */
+} kvshot_call;
+
+/* Runs the call described by *call (host struct; device pointers inside). */
+kvshot_status kvshot_draft_attn_call(kvshot_handle h, const kvshot_call* call, void* stream);
+
+/* kvshot_draft_attn_validate for a kvshot_call: also checks query_nodes
+ * (code 5: a node outside [0, n_nodes)) and pos_base (code 6: negative, or a
+ * draft position beyond the RoPE table).  Synchronises `stream`. */
+kvshot_status kvshot_draft_attn_validate_call(kvshot_handle h, const kvshot_call* call, int32_t* first_bad,
+                                              void* stream);
+
 /* Checks device-side contract data for a call with these sizes: every page id a
  * call would read lies in [0, num_pages), 0 <= ctx_lens[b] <= max_ctx_len_hint,
  * step offsets in range (if step_offsets != NULL), parents in {-1} U [0, i)

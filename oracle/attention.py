@@ -169,7 +169,7 @@ def _memory_attention(qrot, Kt, Vt, dk_rot, dv, allowed_draft, num_kv_heads, sca
 
 def draft_attention_step(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, step_offsets, *,
                          dtype: str, page_size: int, rope_theta: float = 1e6, softmax_scale: float = 0.0,
-                         seqs: Optional[Iterable[int]] = None):
+                         seqs: Optional[Iterable[int]] = None, pos_base=None):
     """Causal draft steps.  Returns (out ``[B][n][Hq][D]``, lse ``[B][n][Hq]``) in float64.
 
     Readings where the paper is silent:
@@ -182,6 +182,8 @@ def draft_attention_step(q, k_pages, v_pages, page_table, ctx_lens, draft_k, dra
         included);
       * scale 1/sqrt(D) unless ``softmax_scale`` is non-zero.
     ``seqs`` restricts the computation to some sequences (other rows are NaN).
+    ``pos_base[b]``, when given, replaces T_b as the position of draft step 0
+    (the prefix keys are used as stored either way).
     """
     q = np.asarray(q)
     B, n, Hq, D = q.shape
@@ -195,8 +197,9 @@ def draft_attention_step(q, k_pages, v_pages, page_table, ctx_lens, draft_k, dra
         S = s0 + n
         Kt = decode(gather_prefix(k_pages, page_table[b], T, page_size), dtype)
         Vt = decode(gather_prefix(v_pages, page_table[b], T, page_size), dtype)
-        qpos = T + s0 + np.arange(n)
-        kpos = T + np.arange(S)
+        base = T if pos_base is None else int(pos_base[b])
+        qpos = base + s0 + np.arange(n)
+        kpos = base + np.arange(S)
         qrot = rope(decode(q[b], dtype), qpos[:, None], rope_theta)
         dk = rope(decode(draft_k[b, :S], dtype), kpos[:, None], rope_theta)
         dv = decode(draft_v[b, :S], dtype)
@@ -207,32 +210,37 @@ def draft_attention_step(q, k_pages, v_pages, page_table, ctx_lens, draft_k, dra
 
 def draft_attention_tree(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, parents, *,
                          dtype: str, page_size: int, rope_theta: float = 1e6, softmax_scale: float = 0.0,
-                         seqs: Optional[Iterable[int]] = None):
-    """Tree drafting.  Returns (out ``[B][N][Hq][D]``, lse ``[B][N][Hq]``) in float64.
+                         seqs: Optional[Iterable[int]] = None, query_nodes=None, pos_base=None):
+    """Tree drafting.  Returns (out ``[B][n_q][Hq][D]``, lse ``[B][n_q][Hq]``) in float64.
 
     Readings: node i of sequence b sits at position T_b + depth(i) (roots at
     T_b); draft key s (the key of node s) is rotated at T_b + depth(s); node i
     sees every target key and the keys of its ancestors and itself; parents[i]
-    is -1 (root, forests allowed) or an earlier node.
+    is -1 (root, forests allowed) or an earlier node.  ``parents`` is
+    [B][N] over all N nodes; query row j is node ``query_nodes[b][j]`` when
+    given (a tree grown level by level queries its newest level only), else
+    node j.  ``pos_base[b]``, when given, replaces T_b as the position of depth 0.
     """
     q = np.asarray(q)
-    B, N, Hq, D = q.shape
+    B, nq, Hq, D = q.shape
+    N = np.asarray(parents).shape[1]
     Hkv = k_pages.shape[1]
     scale = softmax_scale if softmax_scale != 0.0 else 1.0 / math.sqrt(D)
-    out = np.full((B, N, Hq, D), np.nan)
-    lse = np.full((B, N, Hq), np.nan)
+    out = np.full((B, nq, Hq, D), np.nan)
+    lse = np.full((B, nq, Hq), np.nan)
     for b in (range(B) if seqs is None else seqs):
         T = int(ctx_lens[b])
         anc, depth = tree_ancestry(parents[b])
+        nodes = np.arange(nq) if query_nodes is None else np.asarray(query_nodes[b], dtype=np.int64)
         Kt = decode(gather_prefix(k_pages, page_table[b], T, page_size), dtype)
         Vt = decode(gather_prefix(v_pages, page_table[b], T, page_size), dtype)
-        pos = T + depth
-        qrot = rope(decode(q[b], dtype), pos[:, None], rope_theta)
-        dk = rope(decode(draft_k[b, :N], dtype), pos[:, None], rope_theta)
+        base = T if pos_base is None else int(pos_base[b])
+        qrot = rope(decode(q[b], dtype), (base + depth[nodes])[:, None], rope_theta)
+        dk = rope(decode(draft_k[b, :N], dtype), (base + depth)[:, None], rope_theta)
         dv = decode(draft_v[b, :N], dtype)
-        allowed = np.zeros((N, N), dtype=bool)
-        for i in range(N):
-            allowed[i, sorted(anc[i])] = True
+        allowed = np.zeros((nq, N), dtype=bool)
+        for j, i in enumerate(nodes):
+            allowed[j, sorted(anc[int(i)])] = True
         out[b], lse[b] = _memory_attention(qrot, Kt, Vt, dk, dv, allowed, Hkv, scale)
     return out, lse
 
@@ -241,8 +249,10 @@ def draft_attention(case, seqs: Optional[Iterable[int]] = None):
     """Dispatch on a case object exposing the call's arrays as attributes."""
     common = dict(dtype=case.dtype, page_size=case.page_size, rope_theta=case.rope_theta,
                   softmax_scale=case.softmax_scale, seqs=seqs)
+    pos_base = getattr(case, "pos_base", None)
     if case.mode == "step":
         return draft_attention_step(case.q, case.k_pages, case.v_pages, case.page_table, case.ctx_lens,
-                                    case.draft_k, case.draft_v, case.step_offsets, **common)
+                                    case.draft_k, case.draft_v, case.step_offsets, pos_base=pos_base, **common)
     return draft_attention_tree(case.q, case.k_pages, case.v_pages, case.page_table, case.ctx_lens,
-                                case.draft_k, case.draft_v, case.parents, **common)
+                                case.draft_k, case.draft_v, case.parents, pos_base=pos_base,
+                                query_nodes=getattr(case, "query_nodes", None), **common)

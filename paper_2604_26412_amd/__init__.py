@@ -27,7 +27,7 @@ EXPORTED_SYMBOLS = [
     "kvshot_draft_attn_init", "kvshot_draft_attn_destroy", "kvshot_draft_attn_step", "kvshot_draft_attn_tree",
     "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
     "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_debug_stream_read",
-    "kvshot_status_string",
+    "kvshot_status_string", "kvshot_draft_attn_call", "kvshot_draft_attn_validate_call",
     "kvshot_fusion_init", "kvshot_fusion_destroy", "kvshot_gated_delta_fusion", "kvshot_fusion_set_option",
     "kvshot_fusion_plan", "kvshot_fusion_profile_read", "kvshot_fusion_pack_weights",
     "kvshot_gated_delta_fusion_packed",
@@ -43,6 +43,21 @@ class KvshotConfig(ctypes.Structure):
         ("num_pages", ctypes.c_int32), ("max_position", ctypes.c_int64), ("rope_theta", ctypes.c_double),
         ("softmax_scale", ctypes.c_float), ("reserved", ctypes.c_int32), ("page_stride", ctypes.c_int64),
         ("head_stride", ctypes.c_int64), ("slot_stride", ctypes.c_int64),
+    ]
+
+
+MODE_STEP, MODE_TREE = 0, 1
+
+
+class KvshotCall(ctypes.Structure):
+    _fields_ = [
+        ("mode", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_queries", ctypes.c_int32),
+        ("n_nodes", ctypes.c_int32), ("max_ctx_len_hint", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("q", ctypes.c_void_p), ("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+        ("page_table", ctypes.c_void_p), ("ctx_lens", ctypes.c_void_p), ("draft_k", ctypes.c_void_p),
+        ("draft_v", ctypes.c_void_p), ("step_offsets", ctypes.c_void_p), ("parents", ctypes.c_void_p),
+        ("query_nodes", ctypes.c_void_p), ("pos_base", ctypes.c_void_p), ("out", ctypes.c_void_p),
+        ("lse", ctypes.c_void_p),
     ]
 
 
@@ -80,6 +95,8 @@ def load_library(path: Optional[str] = None):
         "kvshot_debug_gather_kv": [_vp, _i32, _i32] + [_vp] * 7,
         "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
         "kvshot_debug_stream_read": [_vp, _i64, _vp, _i32, _vp],
+        "kvshot_draft_attn_call": [_vp, ctypes.POINTER(KvshotCall), _vp],
+        "kvshot_draft_attn_validate_call": [_vp, ctypes.POINTER(KvshotCall), ctypes.POINTER(_i32), _vp],
         "kvshot_fusion_init": [_i32, _i32, ctypes.POINTER(_vp)],
         "kvshot_fusion_destroy": [_vp],
         "kvshot_gated_delta_fusion": [_vp, _i32] + [_vp] * 7 + [_i32, _vp],
@@ -233,26 +250,66 @@ class DraftAttention:
 
     # -- calls -------------------------------------------------------------
     def step(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, step_offsets, *, max_ctx=None,
-             out=None, lse=None, stream=None):
-        """Causal draft steps; returns ``out`` [B][n_new][Hq][D]."""
+             out=None, lse=None, pos_base=None, stream=None):
+        """Causal draft steps; returns ``out`` [B][n_new][Hq][D].
+
+        ``pos_base`` (int32 [B]) places draft step 0 of sequence b at position pos_base[b] instead of
+        ctx_lens[b] (see ``kvshot_call`` in the header).
+        """
         torch = _torch()
         ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
-        offs = self._tensor(step_offsets, "step_offsets", torch.int32, (q.shape[0],))
-        _check("kvshot_draft_attn_step", self._lib.kvshot_draft_attn_step(
-            self._h, q.shape[0], q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
-            ptrs["lens"], ptrs["dk"], ptrs["dv"], offs, ptrs["out"], ptrs["lse"], self._stream(stream)))
+        B = q.shape[0]
+        offs = self._tensor(step_offsets, "step_offsets", torch.int32, (B,))
+        if pos_base is None:
+            _check("kvshot_draft_attn_step", self._lib.kvshot_draft_attn_step(
+                self._h, B, q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
+                ptrs["lens"], ptrs["dk"], ptrs["dv"], offs, ptrs["out"], ptrs["lse"], self._stream(stream)))
+            return out
+        call = self._call(MODE_STEP, q, q.shape[1], 0, max_ctx, ptrs, pos_base)
+        call.step_offsets = offs
+        _check("kvshot_draft_attn_call", self._lib.kvshot_draft_attn_call(self._h, ctypes.byref(call),
+                                                                         self._stream(stream)))
         return out
 
     def tree(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, parents, *, max_ctx=None,
-             out=None, lse=None, stream=None):
-        """Draft-tree nodes with an ancestor-or-self mask; returns ``out`` [B][n_nodes][Hq][D]."""
+             out=None, lse=None, query_nodes=None, pos_base=None, stream=None):
+        """Draft-tree queries with an ancestor-or-self mask; returns ``out`` [B][n_queries][Hq][D].
+
+        ``parents`` is [B][n_nodes]; without ``query_nodes`` every node has a query row (n_queries ==
+        n_nodes).  ``query_nodes`` (int32 [B][n_queries]) names the node of each query row, so a tree grown
+        level by level needs queries for its newest level only.  ``pos_base`` as in :meth:`step`.
+        """
         torch = _torch()
         ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
-        par = self._tensor(parents, "parents", torch.int32, (q.shape[0], q.shape[1]))
-        _check("kvshot_draft_attn_tree", self._lib.kvshot_draft_attn_tree(
-            self._h, q.shape[0], q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
-            ptrs["lens"], ptrs["dk"], ptrs["dv"], par, ptrs["out"], ptrs["lse"], self._stream(stream)))
+        B, nq = q.shape[0], q.shape[1]
+        n_nodes = parents.shape[1] if parents.dim() == 2 else -1
+        par = self._tensor(parents, "parents", torch.int32, (B, n_nodes))
+        if query_nodes is None and pos_base is None:
+            if n_nodes != nq:
+                raise ValueError("parents must be [B][n_queries] without query_nodes")
+            _check("kvshot_draft_attn_tree", self._lib.kvshot_draft_attn_tree(
+                self._h, B, nq, self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
+                ptrs["lens"], ptrs["dk"], ptrs["dv"], par, ptrs["out"], ptrs["lse"], self._stream(stream)))
+            return out
+        call = self._call(MODE_TREE, q, nq, n_nodes, max_ctx, ptrs, pos_base)
+        call.parents = par
+        if query_nodes is not None:
+            call.query_nodes = self._tensor(query_nodes, "query_nodes", torch.int32, (B, nq))
+        _check("kvshot_draft_attn_call", self._lib.kvshot_draft_attn_call(self._h, ctypes.byref(call),
+                                                                         self._stream(stream)))
         return out
+
+    def _call(self, mode, q, nq, n_nodes, max_ctx, ptrs, pos_base):
+        torch = _torch()
+        c = KvshotCall()
+        c.mode, c.batch, c.n_queries, c.n_nodes = mode, q.shape[0], nq, n_nodes
+        c.max_ctx_len_hint, c.reserved = self._hint(max_ctx), 0
+        c.q, c.k_pages, c.v_pages = ptrs["q"], ptrs["k"], ptrs["v"]
+        c.page_table, c.ctx_lens, c.draft_k, c.draft_v = ptrs["pt"], ptrs["lens"], ptrs["dk"], ptrs["dv"]
+        c.out, c.lse = ptrs["out"], ptrs["lse"]
+        if pos_base is not None:
+            c.pos_base = self._tensor(pos_base, "pos_base", torch.int32, (q.shape[0],))
+        return c
 
     def validate(self, page_table, ctx_lens, n_queries, *, step_offsets=None, parents=None, max_ctx=None,
                  stream=None):

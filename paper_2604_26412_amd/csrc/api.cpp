@@ -172,17 +172,25 @@ kvshot_status drain_profile(kvshot_ctx* c, bool all) {
   return KVSHOT_OK;
 }
 
-kvshot_status run_call(kvshot_ctx* c, int batch, int nq, int max_ctx, bool tree, const void* q, const void* kp,
-                       const void* vp, const int32_t* pt, const int32_t* lens, const void* dk, const void* dv,
-                       const int32_t* offs_or_parents, void* out, float* lse, void* stream) {
+kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
   if (!c) return KVSHOT_ERR_INVALID_ARG;
   const kvshot_config& g = c->cfg;
+  const bool tree = a.mode == KVSHOT_MODE_TREE;
+  const int batch = a.batch, nq = a.n_queries, max_ctx = a.max_ctx_len_hint;
+  if (a.mode != KVSHOT_MODE_STEP && a.mode != KVSHOT_MODE_TREE) return KVSHOT_ERR_INVALID_ARG;
+  if (a.reserved != 0) return KVSHOT_ERR_INVALID_ARG;
   if (batch < 1 || batch > g.max_batch || nq < 1 || nq > g.max_draft) return KVSHOT_ERR_INVALID_ARG;
+  if (tree && (a.n_nodes < 1 || a.n_nodes > g.max_draft)) return KVSHOT_ERR_INVALID_ARG;
+  if (tree && !a.query_nodes && a.n_nodes != nq) return KVSHOT_ERR_INVALID_ARG;
+  if (!tree && a.query_nodes) return KVSHOT_ERR_INVALID_ARG;
   if (c->group * nq > kMaxRows) return KVSHOT_ERR_UNSUPPORTED;
   if (max_ctx < 0 || (int64_t)max_ctx > (int64_t)g.max_pages_per_seq * g.page_size) return KVSHOT_ERR_INVALID_ARG;
   if ((int64_t)max_ctx + g.max_draft > g.max_position) return KVSHOT_ERR_INVALID_ARG;
-  if (!q || !kp || !vp || !pt || !lens || !dk || !dv || !offs_or_parents || !out) return KVSHOT_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(kp) || !aligned16(vp) || !aligned16(dk) || !aligned16(dv) || !aligned16(out))
+  if (!a.q || !a.k_pages || !a.v_pages || !a.page_table || !a.ctx_lens || !a.draft_k || !a.draft_v || !a.out)
+    return KVSHOT_ERR_INVALID_ARG;
+  if (tree ? !a.parents : !a.step_offsets) return KVSHOT_ERR_INVALID_ARG;
+  if (!aligned16(a.q) || !aligned16(a.k_pages) || !aligned16(a.v_pages) || !aligned16(a.draft_k) ||
+      !aligned16(a.draft_v) || !aligned16(a.out))
     return KVSHOT_ERR_INVALID_ARG;
   if (c->opt_path == 1 && g.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
   kvshot_status st = check_device(c);
@@ -191,18 +199,23 @@ kvshot_status run_call(kvshot_ctx* c, int batch, int nq, int max_ctx, bool tree,
   const Plan pl = make_plan(c, batch, nq, max_ctx);
   AttnParams p;
   fill_params(c, pl, batch, nq, max_ctx, p);
-  p.q = q;
-  p.k_pages = kp;
-  p.v_pages = vp;
-  p.page_table = pt;
-  p.ctx_lens = lens;
-  p.draft_k = dk;
-  p.draft_v = dv;
+  p.q = a.q;
+  p.k_pages = a.k_pages;
+  p.v_pages = a.v_pages;
+  p.page_table = a.page_table;
+  p.ctx_lens = a.ctx_lens;
+  p.draft_k = a.draft_k;
+  p.draft_v = a.draft_v;
   p.tree = tree ? 1 : 0;
-  p.step_offsets = tree ? nullptr : offs_or_parents;
-  p.parents = tree ? offs_or_parents : nullptr;
-  p.out = out;
-  p.lse = lse;
+  p.n_nodes = tree ? a.n_nodes : nq;
+  p.step_offsets = tree ? nullptr : a.step_offsets;
+  p.parents = tree ? a.parents : nullptr;
+  p.query_nodes = tree ? a.query_nodes : nullptr;
+  p.pos_base = a.pos_base;
+  p.out = a.out;
+  p.lse = a.lse;
+  void* out = a.out;
+  float* lse = a.lse;
   hipStream_t s = (hipStream_t)stream;
 
   ProfileSlot* slot = nullptr;
@@ -248,6 +261,40 @@ kvshot_status run_call(kvshot_ctx* c, int batch, int nq, int max_ctx, bool tree,
     ++c->prof_head;
   }
   return KVSHOT_OK;
+}
+
+kvshot_status validate_impl(kvshot_ctx* c, const kvshot_call& a, int32_t* first_bad, void* stream) {
+  if (first_bad) *first_bad = 0;
+  if (!c || !a.page_table || !a.ctx_lens) return KVSHOT_ERR_INVALID_ARG;
+  const kvshot_config& g = c->cfg;
+  const bool tree = a.mode == KVSHOT_MODE_TREE;
+  if (a.mode != KVSHOT_MODE_STEP && a.mode != KVSHOT_MODE_TREE) return KVSHOT_ERR_INVALID_ARG;
+  if (a.batch < 1 || a.batch > g.max_batch || a.n_queries < 1 || a.n_queries > g.max_draft)
+    return KVSHOT_ERR_INVALID_ARG;
+  if (tree && (a.n_nodes < 1 || a.n_nodes > g.max_draft)) return KVSHOT_ERR_INVALID_ARG;
+  if (a.max_ctx_len_hint < 0 || (int64_t)a.max_ctx_len_hint > (int64_t)g.max_pages_per_seq * g.page_size)
+    return KVSHOT_ERR_INVALID_ARG;
+  kvshot_status st = check_device(c);
+  if (st != KVSHOT_OK) return st;
+  const Plan pl = make_plan(c, a.batch, a.n_queries, a.max_ctx_len_hint);
+  AttnParams p;
+  fill_params(c, pl, a.batch, a.n_queries, a.max_ctx_len_hint, p);
+  p.page_table = a.page_table;
+  p.ctx_lens = a.ctx_lens;
+  p.step_offsets = a.step_offsets;
+  p.parents = a.parents;
+  p.tree = tree ? 1 : 0;
+  p.n_nodes = tree ? a.n_nodes : a.n_queries;
+  p.query_nodes = tree ? a.query_nodes : nullptr;
+  p.pos_base = a.pos_base;
+  hipStream_t s = (hipStream_t)stream;
+  if (launch_validate(p, a.max_ctx_len_hint, c->flag, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
+  int32_t flag = 0;
+  if (hipMemcpyAsync(&flag, c->flag, sizeof(flag), hipMemcpyDeviceToHost, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
+  if (hipStreamSynchronize(s) != hipSuccess) return KVSHOT_ERR_DEVICE;
+  if (flag == 0x7fffffff) return KVSHOT_OK;
+  if (first_bad) *first_bad = flag;
+  return KVSHOT_ERR_DATA;
 }
 
 void free_ctx(kvshot_ctx* c) {
@@ -362,8 +409,22 @@ kvshot_status kvshot_draft_attn_step(kvshot_handle h, int32_t batch, int32_t n_n
                                      const int32_t* page_table, const int32_t* ctx_lens, const void* draft_k,
                                      const void* draft_v, const int32_t* step_offsets, void* out, float* lse,
                                      void* stream) {
-  return run_call(h, batch, n_new, max_ctx_len_hint, false, q, k_pages, v_pages, page_table, ctx_lens, draft_k,
-                  draft_v, step_offsets, out, lse, stream);
+  kvshot_call a{};
+  a.mode = KVSHOT_MODE_STEP;
+  a.batch = batch;
+  a.n_queries = n_new;
+  a.max_ctx_len_hint = max_ctx_len_hint;
+  a.q = q;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.page_table = page_table;
+  a.ctx_lens = ctx_lens;
+  a.draft_k = draft_k;
+  a.draft_v = draft_v;
+  a.step_offsets = step_offsets;
+  a.out = out;
+  a.lse = lse;
+  return run_call(h, a, stream);
 }
 
 kvshot_status kvshot_draft_attn_tree(kvshot_handle h, int32_t batch, int32_t n_nodes, int32_t max_ctx_len_hint,
@@ -371,37 +432,52 @@ kvshot_status kvshot_draft_attn_tree(kvshot_handle h, int32_t batch, int32_t n_n
                                      const int32_t* page_table, const int32_t* ctx_lens, const void* draft_k,
                                      const void* draft_v, const int32_t* parents, void* out, float* lse,
                                      void* stream) {
-  return run_call(h, batch, n_nodes, max_ctx_len_hint, true, q, k_pages, v_pages, page_table, ctx_lens, draft_k,
-                  draft_v, parents, out, lse, stream);
+  kvshot_call a{};
+  a.mode = KVSHOT_MODE_TREE;
+  a.batch = batch;
+  a.n_queries = n_nodes;
+  a.n_nodes = n_nodes;
+  a.max_ctx_len_hint = max_ctx_len_hint;
+  a.q = q;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.page_table = page_table;
+  a.ctx_lens = ctx_lens;
+  a.draft_k = draft_k;
+  a.draft_v = draft_v;
+  a.parents = parents;
+  a.out = out;
+  a.lse = lse;
+  return run_call(h, a, stream);
+}
+
+kvshot_status kvshot_draft_attn_call(kvshot_handle h, const kvshot_call* call, void* stream) {
+  if (!call) return KVSHOT_ERR_INVALID_ARG;
+  return run_call(h, *call, stream);
 }
 
 kvshot_status kvshot_draft_attn_validate(kvshot_handle h, int32_t batch, int32_t n_queries, int32_t max_ctx_len_hint,
                                          const int32_t* page_table, const int32_t* ctx_lens,
                                          const int32_t* step_offsets, const int32_t* parents, int32_t* first_bad,
                                          void* stream) {
+  kvshot_call a{};
+  a.mode = parents ? KVSHOT_MODE_TREE : KVSHOT_MODE_STEP;
+  a.batch = batch;
+  a.n_queries = n_queries;
+  a.n_nodes = n_queries;
+  a.max_ctx_len_hint = max_ctx_len_hint;
+  a.page_table = page_table;
+  a.ctx_lens = ctx_lens;
+  a.step_offsets = step_offsets;
+  a.parents = parents;
+  return validate_impl(h, a, first_bad, stream);
+}
+
+kvshot_status kvshot_draft_attn_validate_call(kvshot_handle h, const kvshot_call* call, int32_t* first_bad,
+                                              void* stream) {
   if (first_bad) *first_bad = 0;
-  if (!h || !page_table || !ctx_lens) return KVSHOT_ERR_INVALID_ARG;
-  const kvshot_config& g = h->cfg;
-  if (batch < 1 || batch > g.max_batch || n_queries < 1 || n_queries > g.max_draft) return KVSHOT_ERR_INVALID_ARG;
-  if (max_ctx_len_hint < 0 || (int64_t)max_ctx_len_hint > (int64_t)g.max_pages_per_seq * g.page_size)
-    return KVSHOT_ERR_INVALID_ARG;
-  kvshot_status st = check_device(h);
-  if (st != KVSHOT_OK) return st;
-  const Plan pl = make_plan(h, batch, n_queries, max_ctx_len_hint);
-  AttnParams p;
-  fill_params(h, pl, batch, n_queries, max_ctx_len_hint, p);
-  p.page_table = page_table;
-  p.ctx_lens = ctx_lens;
-  p.step_offsets = step_offsets;
-  p.parents = parents;
-  hipStream_t s = (hipStream_t)stream;
-  if (launch_validate(p, max_ctx_len_hint, h->flag, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  int32_t flag = 0;
-  if (hipMemcpyAsync(&flag, h->flag, sizeof(flag), hipMemcpyDeviceToHost, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  if (hipStreamSynchronize(s) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  if (flag == 0x7fffffff) return KVSHOT_OK;
-  if (first_bad) *first_bad = flag;
-  return KVSHOT_ERR_DATA;
+  if (!call) return KVSHOT_ERR_INVALID_ARG;
+  return validate_impl(h, *call, first_bad, stream);
 }
 
 kvshot_status kvshot_draft_attn_set_option(kvshot_handle h, int32_t option, int64_t value) {

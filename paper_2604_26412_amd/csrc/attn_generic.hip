@@ -67,7 +67,7 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(AttnParams p) {
   const int key_end = min(key_beg + p.blocks_per_split * kBlockKeys, T);
   const bool last = split == p.splits - 1;
 
-  int s0 = 0, S = p.nq;
+  int s0 = 0, S = p.tree ? p.n_nodes : p.nq;
   if (!p.tree) {
     s0 = p.step_offsets[b];
     s0 = s0 < 0 ? 0 : (s0 > p.max_draft - p.nq ? p.max_draft - p.nq : s0);
@@ -75,7 +75,8 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(AttnParams p) {
   }
   uint64_t anc_mine = 0;
   int depth_mine = 0;
-  if (p.tree) anc_mine = tree_ancestry_wave(p.parents + (int64_t)b * p.nq, p.nq, lane, &depth_mine);
+  if (p.tree) anc_mine = tree_ancestry_wave(p.parents + (int64_t)b * p.n_nodes, p.n_nodes, lane, &depth_mine);
+  const int P = position_base(p, b, T);            // position of draft step 0 / tree depth 0
 
   const int pmask = (1 << p.page_shift) - 1;
   const int64_t row = (int64_t)b * p.max_pages_per_seq;
@@ -90,11 +91,12 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(AttnParams p) {
     uint64_t row_anc = 0;
     int qpos;
     if (p.tree) {
-      const uint32_t lo = __shfl((uint32_t)anc_mine, j), hi = __shfl((uint32_t)(anc_mine >> 32), j);
+      const int node = query_node(p, b, j);
+      const uint32_t lo = __shfl((uint32_t)anc_mine, node), hi = __shfl((uint32_t)(anc_mine >> 32), node);
       row_anc = ((uint64_t)hi << 32) | lo;
-      qpos = T + __shfl(depth_mine, j);
+      qpos = P + __shfl(depth_mine, node);
     } else {
-      qpos = T + s0 + j;
+      qpos = P + s0 + j;
     }
     qpos = qpos >= p.max_position ? p.max_position - 1 : qpos;
 
@@ -139,7 +141,7 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(AttnParams p) {
         load8<BF16>(p.draft_k, off + c * 8, kx);
         load8<BF16>(p.draft_k, off + (c ^ 8) * 8, kp);
         load8<BF16>(p.draft_v, off + c * 8, vx);
-        int kpos = p.tree ? T + __shfl(depth_mine, s) : T + s;
+        int kpos = p.tree ? P + __shfl(depth_mine, s) : P + s;
         kpos = kpos >= p.max_position ? p.max_position - 1 : kpos;
         rope8(kx, kp, c, p.rope + (int64_t)kpos * kHalfDim, kr);
         float part = 0.0f;

@@ -144,8 +144,10 @@ __device__ __forceinline__ void softmax_front(const f32x16& s, SoftmaxState& st,
   bm = fmaxf(bm, __shfl_xor(bm, 32));
   const bool jump = bm > st.m + kRescaleSlack;   // false while both are -inf
   const float mn = jump ? bm : st.m;
-  alpha = __builtin_amdgcn_exp2f(st.m - mn);      // 1 without a jump, 0 when the old max was -inf
   const float mu = mn == -INFINITY ? 0.0f : mn;
+  // 1 without a jump, 0 when the old max was -inf (also while every score so
+  // far, this block's included, is masked: then -inf - (-inf) must not occur)
+  alpha = __builtin_amdgcn_exp2f(st.m - mu);
   float ps = 0.0f;
 #pragma unroll
   for (int v = 0; v < 16; v += 2) {
@@ -210,13 +212,14 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   const int nt = blk1 > blk0 ? blk1 - blk0 : 0;
   const bool last = split == p.splits - 1;
 
-  int s0 = 0, S = p.nq;
+  int s0 = 0, S = p.tree ? p.n_nodes : p.nq;
   if (!p.tree) {
     s0 = p.step_offsets[b];
     s0 = s0 < 0 ? 0 : (s0 > p.max_draft - p.nq ? p.max_draft - p.nq : s0);
     S = s0 + p.nq;
   }
   const int nd = last ? (S + kBlockKeys - 1) / kBlockKeys : 0;
+  const int P = position_base(p, b, T);            // position of draft step 0 / tree depth 0
 
   uint16_t* ktile = (uint16_t*)(lds + ks * kBufs * kStreamBytes);
   uint16_t* vtile = (uint16_t*)(lds + ks * kBufs * kStreamBytes + kKTileBytes);
@@ -307,7 +310,7 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   // ---- query rows of this lane: tile rt * TPW + i holds rows (rg * RT + rt * TPW + i) * 32 + lane % 32 ----
   uint64_t anc_mine = 0;
   int depth_mine = 0;
-  if (p.tree) anc_mine = tree_ancestry_wave(p.parents + (int64_t)b * p.nq, p.nq, lane, &depth_mine);
+  if (p.tree) anc_mine = tree_ancestry_wave(p.parents + (int64_t)b * p.n_nodes, p.n_nodes, lane, &depth_mine);
   int r[TPW], jrow[TPW], hqr[TPW];
   bool row_ok[TPW];
   uint64_t row_anc[TPW];
@@ -323,11 +326,12 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
     int qpos;
     row_anc[i] = 0;
     if (p.tree) {
-      const uint32_t lo = __shfl((uint32_t)anc_mine, jrow[i]), hi = __shfl((uint32_t)(anc_mine >> 32), jrow[i]);
+      const int node = query_node(p, b, jrow[i]);
+      const uint32_t lo = __shfl((uint32_t)anc_mine, node), hi = __shfl((uint32_t)(anc_mine >> 32), node);
       row_anc[i] = ((uint64_t)hi << 32) | lo;
-      qpos = T + __shfl(depth_mine, jrow[i]);
+      qpos = P + __shfl(depth_mine, node);
     } else {
-      qpos = T + s0 + jrow[i];
+      qpos = P + s0 + jrow[i];
     }
     qpos = qpos >= p.max_position ? p.max_position - 1 : qpos;
     // query operand: rotated, scaled into log2 units, bf16 (hi/lo pair when split)
@@ -535,7 +539,7 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
 #pragma unroll
         for (int kc = 0; kc < 8; ++kc) kraw[kc] = *(const u32x4*)(ktile + k_rd + kc * 16);
         const int sk = min(key0 + kperm, S - 1);
-        int kpos = p.tree ? T + __shfl(depth_mine, sk & 63) : T + sk;
+        int kpos = p.tree ? P + __shfl(depth_mine, sk & 63) : P + sk;
         kpos = kpos >= p.max_position ? p.max_position - 1 : kpos;
         bf16x8 kop[8];
         rope_rotate_to_bf16(kraw, p.rope + (int64_t)kpos * kHalfDim + hh * 8, 1.0f, kop);

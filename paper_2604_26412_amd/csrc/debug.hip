@@ -57,9 +57,30 @@ __global__ __launch_bounds__(256) void validate_kernel(AttnParams p, int max_ctx
     const int s0 = p.step_offsets[b];
     if (s0 < 0 || s0 + p.nq > p.max_draft) atomicMin(flag, 3);
   }
-  if (p.parents && t < p.nq) {
-    const int par = p.parents[(int64_t)b * p.nq + t];
+  if (p.parents && t < p.n_nodes) {
+    const int par = p.parents[(int64_t)b * p.n_nodes + t];
     if (par < -1 || par >= t) atomicMin(flag, 4);
+  }
+  if (p.query_nodes && t < p.nq) {
+    const int node = p.query_nodes[(int64_t)b * p.nq + t];
+    if (node < 0 || node >= p.n_nodes) atomicMin(flag, 5);
+  }
+  if (p.pos_base && t < 64) {
+    // the highest position this sequence's draft queries and keys use must have a RoPE table entry
+    const int base = p.pos_base[b];
+    int top = 0;
+    if (p.tree) {
+      int depth = 0;
+      (void)tree_ancestry_wave(p.parents + (int64_t)b * p.n_nodes, p.n_nodes, t, &depth);
+      top = depth;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) top = max(top, __shfl_xor(top, o));
+    } else {
+      int s0 = p.step_offsets ? p.step_offsets[b] : 0;
+      s0 = s0 < 0 ? 0 : s0;
+      top = s0 + p.nq - 1;
+    }
+    if (t == 0 && (base < 0 || (int64_t)base + top >= p.max_position)) atomicMin(flag, 6);
   }
 }
 

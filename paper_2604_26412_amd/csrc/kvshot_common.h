@@ -27,7 +27,9 @@ struct AttnParams {
   const void* draft_k;          // [B][max_draft][Hkv][D]
   const void* draft_v;
   const int32_t* step_offsets;  // [B] (step mode) or null
-  const int32_t* parents;       // [B][nq] (tree mode) or null
+  const int32_t* parents;       // [B][n_nodes] (tree mode) or null
+  const int32_t* query_nodes;   // [B][nq] tree node of each query row, or null (row j is node j)
+  const int32_t* pos_base;      // [B] position of draft step 0 / tree depth 0, or null (the prefix length)
   const float2* rope;           // [max_position][64] (cos, sin)
   void* out;                    // [B][nq][Hq][D]
   float* lse;                   // [B][nq][Hq] or null
@@ -41,6 +43,7 @@ struct AttnParams {
   int32_t row_groups;           // workgroups sharing one (sequence, KV head, split), each with its own rows
   int32_t max_position;
   int32_t tree;                 // 0 step, 1 tree
+  int32_t n_nodes;              // tree mode: draft-tree nodes (draft keys) per sequence
   int32_t out_fp32;
   float qscale;                 // softmax scale * log2(e): scores come out in log2 units
 };
@@ -140,6 +143,22 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
 #endif
   if ((n & 7) != 0) return id;
   return (id & 7) * (n >> 3) + (id >> 3);
+}
+
+// Position of draft step 0 (tree depth 0) of sequence b: the caller's
+// pos_base[b] when given (clamped to [0, max_position]; positions are clamped
+// to the RoPE table again where used), else the prefix length T.
+__device__ __forceinline__ int position_base(const AttnParams& p, int b, int T) {
+  if (!p.pos_base) return T;
+  const int v = p.pos_base[b];
+  return v < 0 ? 0 : (v > p.max_position ? p.max_position : v);
+}
+
+// Tree node whose query sits in query row j of sequence b (clamped to the tree).
+__device__ __forceinline__ int query_node(const AttnParams& p, int b, int j) {
+  if (!p.query_nodes) return j;
+  const int v = p.query_nodes[(int64_t)b * p.nq + j];
+  return v < 0 ? 0 : (v >= p.n_nodes ? p.n_nodes - 1 : v);
 }
 
 // Element offset of draft row s of sequence b, KV head h.

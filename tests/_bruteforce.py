@@ -61,8 +61,10 @@ def brute_step(case):
     Hkv = c.num_kv_heads
     G = Hq // Hkv
     out = [[[None] * Hq for _ in range(n)] for _ in range(B)]
+    pb = getattr(c, "pos_base", None)
     for b in range(B):
         T = int(c.ctx_lens[b])
+        base = T if pb is None else int(pb[b])
         s0 = int(c.step_offsets[b])
         for j in range(n):
             for h in range(Hq):
@@ -70,23 +72,27 @@ def brute_step(case):
                 keys = _prefix(c.k_pages, c.page_table[b], T, c.page_size, g, c.dtype)
                 vals = _prefix(c.v_pages, c.page_table[b], T, c.page_size, g, c.dtype)
                 for s in range(s0 + j + 1):
-                    keys.append(_rot(_vec(c.draft_k[b][s][g], c.dtype), T + s, c.rope_theta))
+                    keys.append(_rot(_vec(c.draft_k[b][s][g], c.dtype), base + s, c.rope_theta))
                     vals.append(_vec(c.draft_v[b][s][g], c.dtype))
-                qv = _rot(_vec(c.q[b][j][h], c.dtype), T + s0 + j, c.rope_theta)
+                qv = _rot(_vec(c.q[b][j][h], c.dtype), base + s0 + j, c.rope_theta)
                 out[b][j][h] = _attend(qv, keys, vals, c.scale)
     return out
 
 
 def brute_tree(case):
     c = case
-    B, N, Hq, D = c.q.shape
+    B, nq, Hq, D = c.q.shape
     Hkv = c.num_kv_heads
     G = Hq // Hkv
-    out = [[[None] * Hq for _ in range(N)] for _ in range(B)]
+    pb = getattr(c, "pos_base", None)
+    qn = getattr(c, "query_nodes", None)
+    out = [[[None] * Hq for _ in range(nq)] for _ in range(B)]
     for b in range(B):
         T = int(c.ctx_lens[b])
+        base = T if pb is None else int(pb[b])
         par = [int(p) for p in c.parents[b]]
-        for i in range(N):
+        for row in range(nq):
+            i = row if qn is None else int(qn[b][row])
             anc = _ancestors(par, i)
             for h in range(Hq):
                 g = h // G
@@ -94,8 +100,8 @@ def brute_tree(case):
                 vals = _prefix(c.v_pages, c.page_table[b], T, c.page_size, g, c.dtype)
                 for s in sorted(anc):
                     ds = len(_ancestors(par, s)) - 1
-                    keys.append(_rot(_vec(c.draft_k[b][s][g], c.dtype), T + ds, c.rope_theta))
+                    keys.append(_rot(_vec(c.draft_k[b][s][g], c.dtype), base + ds, c.rope_theta))
                     vals.append(_vec(c.draft_v[b][s][g], c.dtype))
-                qv = _rot(_vec(c.q[b][i][h], c.dtype), T + len(anc) - 1, c.rope_theta)
-                out[b][i][h] = _attend(qv, keys, vals, c.scale)
+                qv = _rot(_vec(c.q[b][row][h], c.dtype), base + len(anc) - 1, c.rope_theta)
+                out[b][row][h] = _attend(qv, keys, vals, c.scale)
     return out

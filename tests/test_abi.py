@@ -136,3 +136,18 @@ def test_fusion_null_handle(lib):
     assert lib.kvshot_fusion_set_option(None, 0, 0) == 1
     assert lib.kvshot_fusion_plan(None, 1, None, None) == 1
     assert lib.kvshot_fusion_destroy(None) == 0
+
+
+def test_call_struct_layout_matches_the_header():
+    # six int32 fields, then thirteen pointers: 24 + 13 * 8 bytes, pointers 8-aligned
+    assert ctypes.sizeof(K.KvshotCall) == 128
+    assert K.KvshotCall.q.offset == 24 and K.KvshotCall.lse.offset == 120
+    text = open(os.path.join(ROOT, "include", "kvshot_draft_attn.h")).read()
+    body = text[text.index("typedef struct kvshot_call {"):text.index("} kvshot_call;")]
+    fields = re.findall(r"^\s*(?:const\s+)?[a-z0-9_]+\s*\*?\s*([a-z_0-9]+);", body, flags=re.M)
+    assert fields == [f for f, _ in K.KvshotCall._fields_]
+
+
+def test_call_rejects_null_struct_and_handle(lib):
+    assert lib.kvshot_draft_attn_call(None, None, None) == 1
+    assert lib.kvshot_draft_attn_validate_call(None, None, None, None) == 1

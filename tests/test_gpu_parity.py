@@ -308,3 +308,15 @@ def test_hip_graph_replay_matches_eager():
             assert torch.equal(lse, eager_lse), rep
             step()                                 # eager work between replays
             torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("n,hq", [(40, 8), (30, 8), (40, 16)])
+@pytest.mark.parametrize("lens", [[0, 5], [33, 0]])
+def test_star_forest_blocks_fully_masked_for_some_rows(n, hq, lens):
+    # every node is a root, so it sees only its own draft key: a key stream whose first block holds none
+    # of a row's visible keys must leave that row's state empty (no -inf - -inf), not NaN
+    parents = np.full((2, n), -1, np.int32)
+    c = W.make_case(mode="tree", batch=2, ctx_lens=lens, n_new=n, num_q_heads=hq, parents=parents,
+                    dtype="bf16", seed=60 + n)
+    for splits in (None, 1):
+        _check_case(c, splits=splits, what=f"star forest n={n} hq={hq} lens={lens} splits={splits}")

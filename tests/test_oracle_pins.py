@@ -338,3 +338,60 @@ def test_reduces_to_torch_sdpa_for_one_sequence():
                       torch.arange(S)[None, :] <= (s0 + torch.arange(n))[:, None]], 1)
     ref = torch.nn.functional.scaled_dot_product_attention(Q, K, V, attn_mask=mask, scale=1 / math.sqrt(D))
     np.testing.assert_allclose(out[0], ref.transpose(0, 1).numpy(), atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# position base and query-node subset (general call: head-concatenated
+# prefixes, level-wise tree growth)
+# ---------------------------------------------------------------------------
+
+def test_pos_base_equal_to_ctx_len_is_the_default_bit_for_bit():
+    c = tiny(ctx_lens=[5, 3], step_offsets=[1, 0], max_draft=5)
+    ref, _ = run(c)
+    c.pos_base = c.ctx_lens.copy()
+    out, _ = run(c)
+    assert np.array_equal(out, ref)
+    t = tiny(mode="tree", n_new=5, parents=np.array([[-1, 0, 0, 1, 2], [-1, 0, 1, -1, 3]], np.int32))
+    ref, _ = run(t)
+    t.pos_base = t.ctx_lens.copy()
+    out, _ = run(t)
+    assert np.array_equal(out, ref)
+
+
+def test_empty_prefix_output_is_invariant_to_the_position_base():
+    # with no prefix every score is draft-draft, and RoPE scores depend only on position differences
+    c = tiny(ctx_lens=[0, 0], step_offsets=[2, 0], max_draft=6)
+    ref, _ = run(c)
+    c.pos_base = np.array([1000, 37], np.int32)
+    out, _ = run(c)
+    np.testing.assert_allclose(out, ref, atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("mode", ["step", "tree"])
+def test_pos_base_matches_bruteforce(mode):
+    if mode == "step":
+        c = tiny(ctx_lens=[6, 2], step_offsets=[1, 2], max_draft=6, head_dim=4, rope_theta=80.0)
+    else:
+        c = tiny(mode="tree", n_new=5, parents=np.array([[-1, 0, 1, 1, 0], [-1, -1, 0, 1, 2]], np.int32),
+                 head_dim=4, rope_theta=60.0, ctx_lens=[5, 3], page_size=4)
+    c.pos_base = np.array([2, 11], np.int32)          # not the prefix lengths
+    out, _ = run(c)
+    bf = np.array(BF.brute_step(c) if mode == "step" else BF.brute_tree(c))
+    np.testing.assert_allclose(out, bf, atol=1e-12, rtol=1e-12)
+
+
+def test_query_node_subset_selects_rows_of_the_full_tree():
+    parents = np.array([[-1, 0, 0, 1, 1, 2, 3], [-1, 0, 1, 2, 0, 4, -1]], np.int32)
+    full = tiny(mode="tree", n_new=7, parents=parents, ctx_lens=[6, 4])
+    ref, ref_lse = run(full)
+    nodes = np.array([[3, 4, 5], [6, 2, 5]], np.int32)      # e.g. the newest level of each tree
+    sub = tiny(mode="tree", n_new=7, parents=parents, ctx_lens=[6, 4])
+    sub.q = np.stack([full.q[b][nodes[b]] for b in range(2)])
+    sub.query_nodes = nodes
+    sub.n_new = 3
+    out, lse = run(sub)
+    for b in range(2):
+        assert np.array_equal(out[b], ref[b][nodes[b]])
+        assert np.array_equal(lse[b], ref_lse[b][nodes[b]])
+    bf = np.array(BF.brute_tree(sub))
+    np.testing.assert_allclose(out, bf, atol=1e-12, rtol=1e-12)

@@ -127,7 +127,9 @@ class DraftCase:
     draft_k: np.ndarray            # [B][max_draft][Hkv][D]  (pre-RoPE)
     draft_v: np.ndarray
     step_offsets: Optional[np.ndarray] = None   # int32 [B] (step mode)
-    parents: Optional[np.ndarray] = None        # int32 [B][n_new] (tree mode)
+    parents: Optional[np.ndarray] = None        # int32 [B][n_nodes] (tree mode; n_nodes == n_new without query_nodes)
+    query_nodes: Optional[np.ndarray] = None    # int32 [B][n_new]: tree node of each query row (tree mode)
+    pos_base: Optional[np.ndarray] = None       # int32 [B]: position of draft step 0 / depth 0 (default ctx_lens)
     rope_theta: float = 1e6
     softmax_scale: float = 0.0                  # 0 -> 1/sqrt(head_dim)
     seed: int = 0
@@ -154,7 +156,7 @@ class DraftCase:
         """Number of draft keys sequence b's queries can see in total."""
         if self.mode == "step":
             return int(self.step_offsets[b]) + self.n_new
-        return self.n_new
+        return int(self.parents.shape[1])
 
 
 def build_pages(seed: int, ctx_lens: Sequence[int], num_kv_heads: int, head_dim: int, page_size: int,
