@@ -36,6 +36,13 @@ Parity status per function:
     open with W_Delta = I gives o, block identity of [n; o; Delta], unit
     Delta selects a column); the cross-only variant (n read as zero) is a
     reading: parity unpinned.
+  * ``kvproj.project_kv`` -- the projected-KV cache builder of KV-only
+    drafters (Sec. 3.2, linear projection of the L_s sampled layers' KV and
+    its RoPE-fix variant; App. A, L_s = 3); pinned (selection matrix returns
+    a layer's KV bit for bit, scalar brute force, closed-form rotation of a
+    unit key, linearity, page-permutation invariance).  The stacking order
+    and the rotation of the projected key at the token's position are
+    readings: parity unpinned against the paper.
 """
 from .attention import (  # noqa: F401
     decode,
@@ -50,3 +57,4 @@ from .attention import (  # noqa: F401
     gather_dense,
 )
 from .fusion import gated_delta_fusion, sigmoid  # noqa: F401,E402
+from .kvproj import project_kv, scatter_tokens, stacked_layers  # noqa: F401,E402

@@ -353,3 +353,119 @@ def fusion_algorithmic(tokens: int, d: int) -> dict:
     acts = 2 * tokens * d * 2 + tokens * d * 2
     flops = 2 * tokens * d * (3 * d) + 2 * tokens * d * d
     return dict(bytes=weights + acts, flops=flops)
+
+
+# ---------------------------------------------------------------------------
+# projected-KV cache builder (KV-only drafters): L_s source layer caches and the
+# tokens whose projected K/V enter the drafter's cache
+# ---------------------------------------------------------------------------
+
+_TID_PPERM, _TID_PNEW, _TID_PWK, _TID_PWV = 5001, 5002, 5003, 5004
+_TID_PSRC = 6_000_000   # + (2 layer + kv) * 100_000 + b
+
+
+@dataclass
+class KvProjCase:
+    """Inputs of one projection call (bf16 bits; pools [page][Hkv][P][D])."""
+    k_src: List[np.ndarray]
+    v_src: List[np.ndarray]
+    page_table: np.ndarray     # int32 [B][max_pages_per_seq], -1 padding
+    ctx_lens: np.ndarray       # int32 [B]
+    token_seq: np.ndarray      # int32 [N]
+    token_pos: np.ndarray      # int32 [N]
+    w_k: np.ndarray            # uint16 [d_kv][L d_kv]
+    w_v: np.ndarray
+    page_size: int
+    rope_theta: float = 1e6
+
+    @property
+    def layers(self) -> int:
+        return len(self.k_src)
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.k_src[0].shape[0])
+
+    @property
+    def num_kv_heads(self) -> int:
+        return int(self.k_src[0].shape[1])
+
+    @property
+    def max_pages_per_seq(self) -> int:
+        return int(self.page_table.shape[1])
+
+    @property
+    def n_tokens(self) -> int:
+        return int(self.token_seq.shape[0])
+
+
+def kvproj_case(*, batch: int, ctx_lens, new_tokens, layers: int = 3, num_kv_heads: int = 8, head_dim: int = 128,
+                page_size: int = 16, seed: int = 3001, shuffle: bool = True, poison: bool = True,
+                rope_theta: float = 1e6) -> KvProjCase:
+    """Source caches of ``layers`` sampled target layers and the tokens to project.
+
+    Sequence b holds ctx_lens[b] tokens in every source layer (N(0, 1) K and V,
+    generated per layer in logical order and scattered through one shared,
+    permuted page table; ~1% spare pages and unused slots hold NaN).  The tokens
+    to project are the last new_tokens[b] positions of each sequence (all of them
+    at prefill), sequence-major.  W_K, W_V ~ N(0, 1 / (layers d_kv)) so the
+    projected vectors have unit scale.
+    """
+    ctx = [int(t) for t in ctx_lens]
+    new = [int(t) for t in new_tokens]
+    assert len(ctx) == batch and len(new) == batch and all(0 <= n <= t for n, t in zip(new, ctx))
+    npages = [-(-t // page_size) for t in ctx]
+    pool = int(sum(npages)) + max(1, int(np.ceil(sum(npages) * 0.01)))
+    perm = rng_for(seed, _TID_PPERM).permutation(pool).astype(np.int32) if shuffle \
+        else np.arange(pool, dtype=np.int32)
+    mpps = max(1, max(npages))
+    table = np.full((batch, mpps), -1, dtype=np.int32)
+    fill = BF16_NAN if poison else np.uint16(0)
+    k_src = [np.full((pool, num_kv_heads, page_size, head_dim), fill, np.uint16) for _ in range(layers)]
+    v_src = [np.full((pool, num_kv_heads, page_size, head_dim), fill, np.uint16) for _ in range(layers)]
+    cursor = 0
+    for b, T in enumerate(ctx):
+        ids = perm[cursor:cursor + npages[b]]
+        cursor += npages[b]
+        table[b, :npages[b]] = ids
+        t = np.arange(T)
+        for layer in range(layers):
+            for kv, pools in ((0, k_src), (1, v_src)):
+                x = f32_to_bf16_bits(_normal(seed, _TID_PSRC + (2 * layer + kv) * 100_000 + b,
+                                             (T, num_kv_heads, head_dim)))
+                pools[layer][ids[t // page_size], :, t % page_size, :] = x
+    seq = np.concatenate([np.full(n, b, np.int32) for b, n in enumerate(new)]) if sum(new) else np.zeros(0, np.int32)
+    pos = np.concatenate([np.arange(t - n, t, dtype=np.int32) for t, n in zip(ctx, new)]) if sum(new) \
+        else np.zeros(0, np.int32)
+    d_kv = num_kv_heads * head_dim
+    sd = np.float32(1.0 / np.sqrt(layers * d_kv))
+    w_k = f32_to_bf16_bits(_normal(seed, _TID_PWK, (d_kv, layers * d_kv)) * sd)
+    w_v = f32_to_bf16_bits(_normal(seed, _TID_PWV, (d_kv, layers * d_kv)) * sd)
+    return KvProjCase(k_src=k_src, v_src=v_src, page_table=table, ctx_lens=np.asarray(ctx, np.int32),
+                      token_seq=seq.astype(np.int32), token_pos=pos.astype(np.int32), w_k=w_k, w_v=w_v,
+                      page_size=page_size, rope_theta=rope_theta)
+
+
+def verify_counts(seed: int, batch: int, hi: int = 8) -> np.ndarray:
+    """Tokens entering the cache after one verification, per sequence: U{1 .. hi} (seeded)."""
+    return rng_for(seed, _TID_PNEW).integers(1, hi + 1, size=batch).astype(np.int32)
+
+
+# Projection workloads: Qwen3-8B KV geometry (8 KV heads x 128, d_kv = 1024), L_s = 3
+# sampled layers (App. A), paged at 16 tokens, 64 sequences of 32K tokens (the
+# long-range attention workload's cache).  The bench builds these on the device.
+KVPROJ_WORKLOADS = {
+    # building the whole projected cache of a 64 x 32K batch (prefill): 2,097,152 tokens
+    "kvproj_prefill_b64_t32k": dict(batch=64, ctx=32768, new="all", seed=3101),
+    # one verification's accepted tokens entering the cache: U{1..8} per sequence
+    "kvproj_verify_b64_t32k": dict(batch=64, ctx=32768, new="verify", seed=3102),
+}
+
+
+def kvproj_algorithmic(n_tokens: int, layers: int = 3, d_kv: int = 1024) -> dict:
+    """Unique bytes (bf16 source vectors, weights, projected output) and flops of one call."""
+    src = 2 * n_tokens * layers * d_kv * 2
+    weights = 2 * d_kv * layers * d_kv * 2
+    out = 2 * n_tokens * d_kv * 2
+    flops = 2 * 2 * n_tokens * d_kv * layers * d_kv
+    return dict(bytes=src + weights + out, flops=flops, src=src, weights=weights, out=out)
