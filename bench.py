@@ -214,12 +214,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", choices=["attention", "fusion"], default="attention",
+    ap.add_argument("--op", choices=["attention", "fusion", "kvproj"], default="attention",
                     help="attention: the draft-step attention path (default); fusion: the hybrid drafter's "
-                         "gated delta fusion")
+                         "gated delta fusion; kvproj: the projected-KV cache builder of KV-only drafters")
     ap.add_argument("--workload", default=None,
                     choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8",
-                             "fusion_t64_d4096", "fusion_t480_d4096"])
+                             "fusion_t64_d4096", "fusion_t480_d4096", "kvproj_prefill_b64_t32k",
+                             "kvproj_verify_b64_t32k"])
+    ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--cold", action="store_true",
@@ -246,6 +248,8 @@ def main():
     torch.cuda.set_device(0)
     if args.op == "fusion":
         return bench_fusion(args, torch, K, W)
+    if args.op == "kvproj":
+        return bench_kvproj(args, torch, K, W)
     if args.workload is None:
         args.workload = DEFAULT_WORKLOAD
     if args.workload.startswith("fusion"):
@@ -595,6 +599,257 @@ def bench_fusion(args, torch, K, W):
         res["parity_sample"] = parity
     print(json.dumps(res), flush=True)
     fz.close()
+
+
+# ---------------------------------------------------------------------------
+# projected-KV cache builder (--op kvproj)
+# ---------------------------------------------------------------------------
+
+KVPROJ_METRIC = "projected-KV cache build tokens/s (L_s=3 layers, d_kv=1024, bf16) with achieved TFLOP/s and HBM GB/s"
+
+
+def kvproj_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kvproj.hip", "kvproj_common.h", "kvshot_common.h"):
+        h.update(open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_kvproj_traffic(workload: str):
+    path = os.path.join(PROFILES, f"kvproj_kernel_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not (m and f and w) or m.group(1) != kvproj_source_hash():
+        return None
+    return float(f.group(1)) + float(w.group(1))
+
+
+def make_kvproj_on_device(torch, W, spec, L=3, Hkv=8, D=128, P=16):
+    """Seeded device-side generator of a projection workload: L source layer pools (N(0, 1) bf16, NaN
+    spare pages) behind one random page table, W_K/W_V ~ N(0, 1/(L d_kv)), and the token list."""
+    B, T, seed = spec["batch"], spec["ctx"], spec["seed"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    pps = T // P
+    used = B * pps
+    pool = used + max(1, used // 100)
+    perm = torch.randperm(pool, generator=g, device="cuda")
+    table = perm[:used].view(B, pps).to(torch.int32).contiguous()
+    spare = perm[used:]
+    pools = []
+    for _ in range(2 * L):
+        x = torch.randn((pool, Hkv, P, D), generator=g, device="cuda", dtype=torch.bfloat16)
+        x[spare] = float("nan")
+        pools.append(x)
+    d_kv = Hkv * D
+    sd = 1.0 / (L * d_kv) ** 0.5
+    w_k = (torch.randn((d_kv, L * d_kv), generator=g, device="cuda") * sd).to(torch.bfloat16)
+    w_v = (torch.randn((d_kv, L * d_kv), generator=g, device="cuda") * sd).to(torch.bfloat16)
+    if spec["new"] == "all":
+        counts = [T] * B
+    else:
+        counts = [int(c) for c in W.verify_counts(seed, B)]
+    seq = torch.cat([torch.full((c,), b, dtype=torch.int32) for b, c in enumerate(counts)])
+    pos = torch.cat([torch.arange(T - c, T, dtype=torch.int32) for c in counts])
+    kd = torch.zeros((pool, Hkv, P, D), device="cuda", dtype=torch.bfloat16)
+    vd = torch.zeros_like(kd)
+    return dict(k_src=pools[:L], v_src=pools[L:], table=table, seq=seq.cuda(), pos=pos.cuda(), seq_host=seq.numpy(),
+                pos_host=pos.numpy(), w_k=w_k, w_v=w_v, k_dst=kd, v_dst=vd, B=B, T=T, P=P, L=L, Hkv=Hkv, pool=pool,
+                pps=pps, n=int(seq.numel()), counts=counts)
+
+
+def kvproj_host_sample(torch, d, pick):
+    """A compact host copy for the tokens `pick` (indices into the token list): their source pages only,
+    behind a table that keeps each token's true position (the oracle rotates at it)."""
+    import numpy as np
+
+    import workloads as W
+
+    def bits(t):
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    seq, pos, P = d["seq_host"][pick], d["pos_host"][pick], d["P"]
+    keys = sorted(set(zip(seq.tolist(), (pos // P).tolist())))
+    slot_of = {k: i for i, k in enumerate(keys)}
+    tab_host = d["table"].cpu().numpy()
+    ids = torch.tensor([int(tab_host[b, lp]) for b, lp in keys], dtype=torch.long, device="cuda")
+    table = np.full((len(keys), d["pps"]), -1, np.int32)
+    for (b, lp), i in slot_of.items():
+        table[i, lp] = i
+    cseq = np.array([slot_of[(int(b), int(p // P))] for b, p in zip(seq, pos)], np.int32)
+    case = W.KvProjCase(k_src=[bits(x[ids]) for x in d["k_src"]], v_src=[bits(x[ids]) for x in d["v_src"]],
+                        page_table=table, ctx_lens=np.zeros(len(keys), np.int32), token_seq=cseq,
+                        token_pos=pos.astype(np.int32), w_k=bits(d["w_k"]), w_v=bits(d["w_v"]), page_size=P)
+    dst = [bits(x[ids]) for x in (d["k_dst"], d["v_dst"])]
+    return case, dst
+
+
+def kvproj_cpu_baseline(torch, d, rope, budget_s=12.0):
+    """Time the float64 projection oracle on whole sampled pages of the workload; compare the GPU cache there."""
+    import numpy as np
+
+    import oracle
+
+    rng = np.random.default_rng(7)
+    n, P = d["n"], d["P"]
+    if n <= 4096:
+        pick = np.arange(n)
+    else:   # whole pages: 16 consecutive tokens of a random page of a random sequence
+        starts = rng.choice(n // P, size=min(2048, n // P), replace=False) * P
+        pick = (starts[:, None] + np.arange(P)[None, :]).ravel()
+    case, dst = kvproj_host_sample(torch, d, pick)
+    w_k = oracle.decode(case.w_k, "bf16")
+    w_v = oracle.decode(case.w_v, "bf16")
+    # timed: the oracle on growing prefixes of the sample until the budget is used
+    done, secs, m = 0, 0.0, min(64, case.n_tokens)
+    K = V = None
+    while done < case.n_tokens and secs < budget_s:
+        sl = slice(done, min(case.n_tokens, done + m))
+        t0 = time.perf_counter()
+        k, v = oracle.project_kv(case.k_src, case.v_src, case.page_table, case.token_seq[sl], case.token_pos[sl],
+                                 w_k, w_v, page_size=P, theta=case.rope_theta, rope_keys=rope, w_dtype=None)
+        secs += time.perf_counter() - t0
+        K = k if K is None else np.concatenate([K, k])
+        V = v if V is None else np.concatenate([V, v])
+        done = sl.stop
+        m *= 2
+    pid = case.token_seq[:done]
+    slot = case.token_pos[:done] % P
+    gk = oracle.decode(dst[0][pid, :, slot, :], "bf16")
+    gv = oracle.decode(dst[1][pid, :, slot, :], "bf16")
+    ref = np.concatenate([K.ravel(), V.ravel()])
+    got = np.concatenate([gk.ravel(), gv.ravel()])
+    diff = got - ref
+    parity = dict(max_abs=float(np.abs(diff).max()), rel_l2=float(np.linalg.norm(diff) / np.linalg.norm(ref)),
+                  elementwise_bound_frac=float((np.abs(diff) / (2.0 ** -8 * np.abs(ref) + 1e-3)).max()),
+                  tokens=int(done))
+    return dict(value=round(done / secs, 1), unit="tokens/s", cores=blas_threads(), kind="oracle",
+                host_cpus=os.cpu_count(), seconds=round(secs, 3),
+                sample=f"{done} tokens of the same workload ({'all listed tokens' if n <= 4096 else 'whole pages of random sequences'}), "
+                       f"float64 NumPy oracle (weights decoded once, outside the timing)"), parity
+
+
+def bench_kvproj(args, torch, K, W):
+    name = args.workload or "kvproj_prefill_b64_t32k"
+    if name not in W.KVPROJ_WORKLOADS:
+        raise SystemExit(f"--op kvproj takes one of {sorted(W.KVPROJ_WORKLOADS)}")
+    spec = W.KVPROJ_WORKLOADS[name]
+    log(f"generating {name} on the device")
+    d = make_kvproj_on_device(torch, W, spec)
+    torch.cuda.synchronize()
+    n, L, Hkv, P = d["n"], d["L"], d["Hkv"], d["P"]
+    rope = not args.no_rope
+    proj = K.KvProjection(num_kv_heads=Hkv, num_layers=L, page_size=P, max_pages_per_seq=d["pps"],
+                          num_pages=d["pool"], max_tokens=n, max_position=d["pps"] * P)
+    if args.splits:
+        proj.set_option(K.OPT_SPLITS, args.splits)
+    plan = proj.plan(n)
+
+    def step():
+        proj(d["k_src"], d["v_src"], d["table"], d["seq"], d["pos"], d["w_k"], d["w_v"], d["k_dst"], d["v_dst"],
+             rope=rope)
+
+    if args.copy_calib_gib > 0:
+        nbytes = int(args.copy_calib_gib * (1 << 30))
+        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
+        del src, dst
+
+    log(f"{n} tokens; plan {plan}; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    run_step = step
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        for _ in range(min(args.warmup, 3)):
+            run_step()
+        torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    proj.set_option(K.OPT_PROFILE, 1)
+    for _ in range(args.steps):
+        step()
+    prof = proj.profile_read()
+    proj.set_option(K.OPT_PROFILE, 0)
+    calls = max(1, prof["calls"])
+    main_ms, comb_ms = prof["main_ms"] / calls, prof["combine_ms"] / calls
+    log(f"step {ms_per_step:.4f} ms; projection kernel {main_ms:.4f} ms; combine {comb_ms:.4f} ms")
+
+    d_kv = Hkv * 128
+    alg = W.kvproj_algorithmic(n, L, d_kv)
+    part_bytes = plan["splits"] * n * 2 * d_kv * 4 if plan["splits"] > 1 else 0
+    # main kernel: source vectors and weights in; the projected cache (one split) or the split partials out
+    main_bytes = alg["src"] + alg["weights"] + (part_bytes if part_bytes else alg["out"])
+    intensity = alg["flops"] / alg["bytes"]
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    tflops = alg["flops"] / (main_ms * 1e-3) / 1e12
+    gbs = main_bytes / (main_ms * 1e-3) / 1e9
+    if intensity >= ridge:
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = read_kvproj_traffic(name) if not (args.splits or args.no_rope) else None
+    roof.update({"kernel": f"kvproj_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)",
+                 "kernel_ms": round(main_ms, 5), "combine_ms": round(comb_ms, 5),
+                 "algorithmic_bytes_per_launch": main_bytes, "flops_per_launch": alg["flops"],
+                 "arithmetic_intensity_flop_per_byte": round(intensity, 1),
+                 "achieved_tflops": round(tflops, 2), "achieved_gbs": round(gbs, 2)})
+    res = {
+        "metric": KVPROJ_METRIC,
+        "value": round(n / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {d['B']} sequences x {d['T']} tokens cached, {n} tokens projected, "
+                               f"L_s {L}, d_kv {d_kv}, pages of {P}, random page table, bf16",
+                   "tokens": n, "layers": L, "d_kv": d_kv, "rope": rope, "splits": plan["splits"],
+                   "workgroups": plan["workgroups"], "launch": "python" if args.no_graph else "hip graph replay"},
+        "roofline": roof,
+        "step_tflops": round(alg["flops"] / (ms_per_step * 1e-3) / 1e12, 2),
+        "step_hbm_gbs": round(alg["bytes"] / (ms_per_step * 1e-3) / 1e9, 2),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cb, parity = kvproj_cpu_baseline(torch, d, rope)
+        res["cpu_baseline"] = cb
+        res["parity_sample"] = parity
+    print(json.dumps(res), flush=True)
+    proj.close()
 
 
 if __name__ == "__main__":

@@ -13,7 +13,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["DraftAttention", "GatedDeltaFusion", "KvshotError", "load_library", "LIB_PATH", "EXPORTED_SYMBOLS"]
+__all__ = ["DraftAttention", "GatedDeltaFusion", "KvProjection", "KvshotError", "load_library", "LIB_PATH",
+           "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
@@ -31,8 +32,11 @@ EXPORTED_SYMBOLS = [
     "kvshot_fusion_init", "kvshot_fusion_destroy", "kvshot_gated_delta_fusion", "kvshot_fusion_set_option",
     "kvshot_fusion_plan", "kvshot_fusion_profile_read", "kvshot_fusion_pack_weights",
     "kvshot_gated_delta_fusion_packed",
+    "kvshot_kvproj_init", "kvshot_kvproj_destroy", "kvshot_kv_project", "kvshot_kv_project_validate",
+    "kvshot_kvproj_set_option", "kvshot_kvproj_plan", "kvshot_kvproj_profile_read",
 ]
 FUSION_CROSS_ONLY, FUSION_OUT_FP32 = 1, 2
+KVPROJ_ROPE = 1
 
 
 class KvshotConfig(ctypes.Structure):
@@ -47,6 +51,17 @@ class KvshotConfig(ctypes.Structure):
 
 
 MODE_STEP, MODE_TREE = 0, 1
+
+
+class KvprojConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+        ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32), ("num_pages", ctypes.c_int32),
+        ("dst_num_pages", ctypes.c_int32), ("max_tokens", ctypes.c_int32), ("max_position", ctypes.c_int64),
+        ("rope_theta", ctypes.c_double), ("page_stride", ctypes.c_int64), ("head_stride", ctypes.c_int64),
+        ("slot_stride", ctypes.c_int64), ("dst_page_stride", ctypes.c_int64), ("dst_head_stride", ctypes.c_int64),
+        ("dst_slot_stride", ctypes.c_int64),
+    ]
 
 
 class KvshotCall(ctypes.Structure):
@@ -105,6 +120,15 @@ def load_library(path: Optional[str] = None):
         "kvshot_gated_delta_fusion_packed": [_vp, _i32] + [_vp] * 6 + [_i32, _vp],
         "kvshot_fusion_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32)],
         "kvshot_fusion_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(_i64)],
+        "kvshot_kvproj_init": [ctypes.POINTER(KvprojConfig), ctypes.POINTER(_vp)],
+        "kvshot_kvproj_destroy": [_vp],
+        "kvshot_kv_project": [_vp, _i32, _i32, ctypes.POINTER(_vp), ctypes.POINTER(_vp)] + [_vp] * 8 + [_i32, _vp],
+        "kvshot_kv_project_validate": [_vp, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_i32),
+                                       ctypes.POINTER(_i32), _vp],
+        "kvshot_kvproj_set_option": [_vp, _i32, _i64],
+        "kvshot_kvproj_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32)],
+        "kvshot_kvproj_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_i64)],
     }
     for name, args in sig.items():
@@ -466,5 +490,106 @@ class GatedDeltaFusion:
     def profile_read(self):
         a, c, k = ctypes.c_double(0), ctypes.c_double(0), _i64(0)
         _check("kvshot_fusion_profile_read", self._lib.kvshot_fusion_profile_read(
+            self._h, ctypes.byref(a), ctypes.byref(c), ctypes.byref(k)))
+        return dict(main_ms=a.value, combine_ms=c.value, calls=k.value)
+
+
+class KvProjection:
+    """Handle for the projected-KV cache builder (C ABI in ``include/kvshot_kvproj.h``).
+
+    For each listed token, ``k' = W_K [k^(1); ...; k^(L_s)]`` (rotated at the
+    token's position with ``rope=True``) and ``v' = W_V [v^(1); ...]`` are
+    written into the destination pools at the token's slot.
+    """
+
+    def __init__(self, *, num_kv_heads: int = 8, head_dim: int = 128, num_layers: int = 3, page_size: int = 16,
+                 max_pages_per_seq: int, num_pages: int, dst_num_pages: Optional[int] = None, max_tokens: int,
+                 max_position: int, rope_theta: float = 1e6):
+        self._lib = load_library()
+        self.cfg = KvprojConfig(num_kv_heads=num_kv_heads, head_dim=head_dim, num_layers=num_layers,
+                                page_size=page_size, max_pages_per_seq=max_pages_per_seq, num_pages=num_pages,
+                                dst_num_pages=dst_num_pages if dst_num_pages is not None else num_pages,
+                                max_tokens=max_tokens, max_position=max_position, rope_theta=rope_theta)
+        h = _vp()
+        _check("kvshot_kvproj_init", self._lib.kvshot_kvproj_init(ctypes.byref(self.cfg), ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            self._lib.kvshot_kvproj_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def _pool(self, t, name, npages):
+        shape = (npages, self.cfg.num_kv_heads, self.cfg.page_size, self.cfg.head_dim)
+        return GatedDeltaFusion._tensor(t, name, _torch().bfloat16, shape)
+
+    def _tables(self, page_table, token_seq, token_pos, dst_page_table):
+        torch = _torch()
+        n = token_seq.shape[0]
+        batch = page_table.shape[0]
+        mp = self.cfg.max_pages_per_seq
+        pt = GatedDeltaFusion._tensor(page_table, "page_table", torch.int32, (batch, mp))
+        dpt = (GatedDeltaFusion._tensor(dst_page_table, "dst_page_table", torch.int32, (batch, mp))
+               if dst_page_table is not None else None)
+        ts = GatedDeltaFusion._tensor(token_seq, "token_seq", torch.int32, (n,))
+        tp = GatedDeltaFusion._tensor(token_pos, "token_pos", torch.int32, (n,))
+        return n, batch, pt, ts, tp, dpt
+
+    def __call__(self, k_src, v_src, page_table, token_seq, token_pos, w_k, w_v, k_dst, v_dst, *,
+                 dst_page_table=None, rope: bool = True, stream=None):
+        """Projects the listed tokens into ``k_dst`` / ``v_dst`` (bf16 pools, written in place)."""
+        torch = _torch()
+        L = self.cfg.num_layers
+        if len(k_src) != L or len(v_src) != L:
+            raise ValueError(f"k_src and v_src must hold {L} pools")
+        n, batch, pt, ts, tp, dpt = self._tables(page_table, token_seq, token_pos, dst_page_table)
+        ks = (_vp * L)(*[self._pool(t, f"k_src[{i}]", self.cfg.num_pages) for i, t in enumerate(k_src)])
+        vs = (_vp * L)(*[self._pool(t, f"v_src[{i}]", self.cfg.num_pages) for i, t in enumerate(v_src)])
+        d_kv = self.cfg.num_kv_heads * self.cfg.head_dim
+        wk = GatedDeltaFusion._tensor(w_k, "w_k", torch.bfloat16, (d_kv, L * d_kv))
+        wv = GatedDeltaFusion._tensor(w_v, "w_v", torch.bfloat16, (d_kv, L * d_kv))
+        kd = self._pool(k_dst, "k_dst", self.cfg.dst_num_pages)
+        vd = self._pool(v_dst, "v_dst", self.cfg.dst_num_pages)
+        s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+        _check("kvshot_kv_project", self._lib.kvshot_kv_project(
+            self._h, n, batch, ks, vs, pt, ts, tp, wk, wv, kd, vd, dpt, KVPROJ_ROPE if rope else 0, s))
+        return k_dst, v_dst
+
+    def validate(self, page_table, token_seq, token_pos, *, dst_page_table=None, stream=None):
+        """(status, first bad token, code): code 1 sequence, 2 position, 3 source page, 4 destination page."""
+        torch = _torch()
+        n, batch, pt, ts, tp, dpt = self._tables(page_table, token_seq, token_pos, dst_page_table)
+        bad, code = _i32(0), _i32(0)
+        st = self._lib.kvshot_kv_project_validate(
+            self._h, n, batch, pt, ts, tp, dpt, ctypes.byref(bad), ctypes.byref(code),
+            stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+        if st not in (KVSHOT_OK, 5):
+            _check("kvshot_kv_project_validate", st)
+        return st, bad.value, code.value
+
+    def set_option(self, option: int, value: int):
+        _check("kvshot_kvproj_set_option", self._lib.kvshot_kvproj_set_option(self._h, option, value))
+
+    def plan(self, n_tokens: int):
+        s, w = _i32(0), _i32(0)
+        _check("kvshot_kvproj_plan", self._lib.kvshot_kvproj_plan(self._h, n_tokens, ctypes.byref(s),
+                                                                  ctypes.byref(w)))
+        return dict(splits=s.value, workgroups=w.value)
+
+    def profile_read(self):
+        a, c, k = ctypes.c_double(0), ctypes.c_double(0), _i64(0)
+        _check("kvshot_kvproj_profile_read", self._lib.kvshot_kvproj_profile_read(
             self._h, ctypes.byref(a), ctypes.byref(c), ctypes.byref(k)))
         return dict(main_ms=a.value, combine_ms=c.value, calls=k.value)

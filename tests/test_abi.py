@@ -151,3 +151,55 @@ def test_call_struct_layout_matches_the_header():
 def test_call_rejects_null_struct_and_handle(lib):
     assert lib.kvshot_draft_attn_call(None, None, None) == 1
     assert lib.kvshot_draft_attn_validate_call(None, None, None, None) == 1
+
+
+def good_proj_cfg(**kw):
+    c = K.KvprojConfig()
+    c.num_kv_heads, c.head_dim, c.num_layers, c.page_size = 8, 128, 3, 16
+    c.max_pages_per_seq, c.num_pages, c.dst_num_pages, c.max_tokens = 16, 64, 64, 512
+    c.max_position, c.rope_theta = 300, 1e6
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=64), 2),
+    (dict(num_kv_heads=0), 1),
+    (dict(num_kv_heads=17), 1),
+    (dict(num_layers=0), 1),
+    (dict(num_layers=5), 1),
+    (dict(page_size=24), 1),
+    (dict(page_size=8), 1),
+    (dict(num_pages=0), 1),
+    (dict(dst_num_pages=0), 1),
+    (dict(max_tokens=0), 1),
+    (dict(max_position=0), 1),
+    (dict(rope_theta=-1.0), 1),
+    (dict(slot_stride=64), 1),
+    (dict(dst_head_stride=12), 1),
+])
+def test_kvproj_init_rejects_bad_configs_before_any_device_call(lib, kw, status):
+    h = ctypes.c_void_p(123)
+    assert lib.kvshot_kvproj_init(ctypes.byref(good_proj_cfg(**kw)), ctypes.byref(h)) == status
+    assert h.value is None
+
+
+def test_kvproj_null_handle(lib):
+    h = ctypes.c_void_p()
+    assert lib.kvshot_kvproj_init(None, ctypes.byref(h)) == 1
+    assert lib.kvshot_kv_project(None, 1, 1, None, None, *([None] * 8), 0, None) == 1
+    assert lib.kvshot_kv_project_validate(None, 1, 1, None, None, None, None, None, None, None) == 1
+    assert lib.kvshot_kvproj_set_option(None, 0, 0) == 1
+    assert lib.kvshot_kvproj_plan(None, 1, None, None) == 1
+    assert lib.kvshot_kvproj_profile_read(None, None, None, None) == 1
+    assert lib.kvshot_kvproj_destroy(None) == 0
+
+
+def test_kvproj_config_struct_layout_matches_the_header():
+    # int32 x8, int64, double, int64 x6
+    assert ctypes.sizeof(K.KvprojConfig) == 8 * 4 + 8 + 8 + 6 * 8
+    text = open(os.path.join(ROOT, "include", "kvshot_kvproj.h")).read()
+    body = text[text.index("typedef struct kvshot_kvproj_config {"):text.index("} kvshot_kvproj_config;")]
+    fields = re.findall(r"^\s*[a-z0-9_]+\s+([a-z_0-9]+);", body, flags=re.M)
+    assert fields == [f for f, _ in K.KvprojConfig._fields_]
