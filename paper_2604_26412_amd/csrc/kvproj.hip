@@ -12,25 +12,31 @@
 // one token and four consecutive channels per register quad.  A workgroup owns
 // 256 channels (two KV heads) x 256 tokens; its four waves own one head x 128
 // tokens each, so the RoPE partners (channel m and m + 64 of a head) sit in
-// the same lane.  The reduction runs over L_s d_kv inputs in chunks of 64:
-// chunk k0 is half of one head of one source layer, so a token's chunk is 128
-// contiguous bytes in the paged pool (gathered through the page table once per
-// workgroup) and a weight row's chunk is 128 contiguous bytes.  Both operands
-// are staged through LDS, double buffered, one barrier per chunk.  Within a
-// chunk, a lane of half h covers reduction indices 32 h .. 32 h + 31 and MFMA
-// k-step s takes 32 h + 8 s .. + 7 from both operands (any pairing of operand
-// slots with reduction indices gives the same sum when A and B agree).
+// the same lane.  The reduction runs over L_s d_kv inputs in chunks of KC
+// (a chunk never straddles a head of a source layer, so a token's chunk is
+// 2 KC contiguous bytes in its page slot; the page walk is done once per
+// workgroup).
 //
-// Epilogue: RoPE in registers (float32, table rows at each token's position),
-// bf16 rounding, a transpose through LDS into [token][channel] rows, and
-// 16-byte stores of each (token, head) row into its destination page slot.
-// With few tokens the reduction is split over workgroups; each writes float32
-// partial sums and kvproj_combine_kernel adds them, rotates and scatters.
+// Operand movement: both tiles go straight from global memory into LDS with
+// global_load_lds_dwordx4 (no register staging, no LDS store instructions),
+// NS stages deep: NS - 1 chunks are in flight while one is computed, one
+// barrier per chunk.  Each load is a wave-wide 1 KB block of LDS, so the rows
+// are unpadded and an XOR swizzle on the load side keeps the fragment reads
+// free of bank conflicts.  A chunk's loads are issued one per four MFMAs of
+// the chunk before it.
+//
+// Epilogue: RoPE on keys in registers (angles reduced in float64, sine and
+// cosine from the hardware units), bf16 rounding, and 8-byte stores into the
+// destination page slots.  With few tokens the reduction is split over
+// workgroups; each writes float32 partial sums and kvproj_combine_kernel adds
+// them, rotates and scatters.
 //
 // Work order: channel tile fastest, then split, token tile, tensor.  The
 // hardware hands workgroup i to XCD i % 8; xcd_remap gives each XCD a
 // contiguous range, so the channel tiles that read one token tile share that
 // XCD's L2.
+#include <type_traits>
+
 #include "kvproj_common.h"
 
 namespace kvshot {
@@ -41,24 +47,73 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kKC = 64;                           // reduction indices per chunk
-constexpr int kPitch = kKC + 8;                   // operand row pitch (bf16): 144 B, rows shift by 4 banks
-constexpr int kOpElems = kProjTile * kPitch;      // one operand tile
-constexpr int kOutPitch = kProjTile + 8;          // output tile row pitch (bf16)
-constexpr int kRows = kProjTile / 32;             // operand rows each thread stages: 32 i + tid / 8
-static_assert(kProjTile * kOutPitch <= 4 * kOpElems, "the output tile reuses the operand buffers");
+#ifndef KVSHOT_KVPROJ_KC
+#define KVSHOT_KVPROJ_KC 32
+#endif
+#ifndef KVSHOT_KVPROJ_NS
+#define KVSHOT_KVPROJ_NS 4
+#endif
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
-template <bool SPLIT>
+// vmcnt(n) with no wait on the other counters (gfx9 encoding: vmcnt bits [3:0] and [15:14])
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Barrier without the memory fence of __syncthreads (which would also wait for
+// the operand prefetches still in flight); the clobber keeps the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// One wave-wide 16-byte load from global memory straight into LDS: lane L's 16 bytes land at
+// `lds` + 16 L (global_load_lds_dwordx4; M0 holds the wave-uniform LDS address, set one wait
+// state ahead).  Issued as inline asm: the compiler's own form makes every later LDS read wait
+// for all such loads in flight (it cannot tell the stages apart), which would serialise the
+// prefetch.  Nothing else in these kernels uses M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_to_lds16(const void* src, const void* lds) {
+  const uint32_t la = (uint32_t)(uintptr_t)(lds_void*)lds;
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(la) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Row swizzle of the LDS operand tiles (rows of KC bf16 = KC / 8 pieces of 16 bytes): piece q
+// of row r is stored in slot q ^ swizzle(r).  Chosen so that 8 or 16 consecutive rows read at
+// one logical piece cover distinct 4-byte bank groups with 32 or 64 banks, and so that it
+// depends on bits 0..4 of r only (a fragment row is 32 i + lane % 32 above a multiple of 32).
+template <int KC>
+__device__ __forceinline__ int swizzle(int r) {
+  if constexpr (KC == 64) return (r ^ ((r >> 3) & 3)) & 7;
+  else if constexpr (KC == 32) return ((r >> 1) ^ (r >> 2)) & 3;
+  else return ((r >> 2) ^ (r >> 3)) & 1;
+}
+
+// KC: reduction indices per chunk; NS: LDS stages (chunks in flight: NS - 1).
+template <bool SPLIT, int KC, int NS>
 __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kOpElems];   // [buffer][weights, tokens]
+  constexpr int kPieces = KC / 8;                   // 16-byte pieces per operand row and chunk
+  constexpr int kRowsPerLoad = 64 / kPieces;        // operand rows one wave-wide 16-byte load covers
+  constexpr int kLoads = kProjTile / kRowsPerLoad / 4;   // loads per wave, operand and chunk
+  constexpr int kStageElems = kProjTile * KC;       // one operand tile (bf16)
+  constexpr int kSteps = KC / 16;                   // MFMA k-steps per chunk
+  static_assert(KC == 16 || KC == 32 || KC == 64, "chunk");
+  static_assert(NS >= 2 && NS * 2 * kStageElems * 2 <= 136 * 1024, "stages fit in LDS");
+  // Operand rows are KC * 2 bytes with no padding.  Piece q of row r sits at physical slot
+  // q ^ swz(r) (see swizzle()): the lanes one LDS cycle serves -- 8 or 16 consecutive rows at
+  // one logical piece -- then hit distinct bank groups.
+  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * 2 * kStageElems];
   __shared__ int64_t t_src[kProjTile];   // source element offset of each token's slot (page, slot)
   __shared__ int64_t t_dst[kProjTile];   // destination element offset
   __shared__ int32_t t_pos[kProjTile];   // position, clamped to the RoPE table
   __shared__ const uint16_t* t_layer[2][kProjMaxLayers];   // source pools [K, V][layer]
+  __shared__ double t_rev[kHalfDim];     // RoPE revolutions per position of channel pair m
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -78,7 +133,7 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
   const int n0 = nt * kProjTile;
   const int d_kv = p.hkv * kHeadDim;
   const int K = p.layers * d_kv;
-  const int nchunks = K / kKC;
+  const int nchunks = K / 64;                     // split boundaries are in 64-wide chunks
   const int cbeg = (int)((int64_t)split * nchunks / p.splits);
   const int cend = (int)((int64_t)(split + 1) * nchunks / p.splits);
 
@@ -94,6 +149,7 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
     t_src[tid] = (int64_t)sp * p.page_stride + (int64_t)slot * p.slot_stride;
     t_dst[tid] = (int64_t)dp * p.dst_page_stride + (int64_t)slot * p.dst_slot_stride;
     t_pos[tid] = t < p.max_position ? t : p.max_position - 1;
+    if (tid < kHalfDim) t_rev[tid] = p.rope_rev[tid];
     if (tid == 0) {   // constant indices: the kernel arguments stay in scalar registers
 #pragma unroll
       for (int l = 0; l < kProjMaxLayers; ++l) {
@@ -104,34 +160,41 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
   }
   __syncthreads();
 
-  const int row = tid >> 3;          // staging row within each group of 32
-  const int piece = (tid & 7) * 8;   // staging element offset within the chunk
-  int64_t soff[kRows];
-  int32_t woff[kRows];
+  // ---- operand loads straight into LDS (global_load_lds_dwordx4: lane L of a load lands at
+  // base + 16 L).  Load j of wave w fills rows kRowsPerLoad (4 w + j) + L / kPieces, physical
+  // slot L % kPieces, so lane L fetches the logical piece that belongs there. ----
+  int64_t soff[kLoads];
+  int32_t woff[kLoads];
 #pragma unroll
-  for (int i = 0; i < kRows; ++i) {
-    soff[i] = t_src[32 * i + row] + piece;
-    const int wrow = mt * kProjTile + 32 * i + row;
-    woff[i] = (wrow < d_kv ? wrow : d_kv - 1) * K + piece;
+  for (int j = 0; j < kLoads; ++j) {
+    const int r = kRowsPerLoad * (kLoads * w + j) + lane / kPieces;
+    const int q = (lane % kPieces) ^ swizzle<KC>(r);
+    soff[j] = t_src[r] + 8 * q;
+    const int wrow = mt * kProjTile + r;
+    woff[j] = (wrow < d_kv ? wrow : d_kv - 1) * K + 8 * q;
   }
   const uint16_t* wsrc = g ? p.w_v : p.w_k;
-
-  u32x4 xr[kRows], wr[kRows];
-  auto gload = [&](int c) {
-    const int k0 = c * kKC;
+  const int nch = (cend - cbeg) * (64 / KC);      // chunks of this split (the split plan counts 64-wide ones)
+  const int k_first = cbeg * 64;
+  // the 2 kLoads loads of chunk c into `stage`: the first kLoads are weight rows, the rest token rows
+  struct Target {
+    const uint16_t* w;    // weight columns of the chunk
+    const uint16_t* x;    // the chunk's head-half of the source layer
+    uint16_t* lds;        // the stage
+  };
+  auto target = [&](int c, int stage) {
+    const int k0 = k_first + c * KC;
     const int l = k0 / d_kv;
     const int rem = k0 - l * d_kv;
-    const uint16_t* src = t_layer[g][l] + (int64_t)(rem >> 7) * p.head_stride + (rem & 127);
-#pragma unroll
-    for (int i = 0; i < kRows; ++i) xr[i] = *(const u32x4*)(src + soff[i]);
-#pragma unroll
-    for (int i = 0; i < kRows; ++i) wr[i] = *(const u32x4*)(wsrc + woff[i] + k0);
+    Target t;
+    t.w = wsrc + k0;
+    t.x = t_layer[g][l] + (int64_t)(rem >> 7) * p.head_stride + (rem & 127);
+    t.lds = smem + stage * 2 * kStageElems + (kLoads * w) * 512;
+    return t;
   };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < kRows; ++i) *(u32x4*)&lds[buf][0][(32 * i + row) * kPitch + piece] = wr[i];
-#pragma unroll
-    for (int i = 0; i < kRows; ++i) *(u32x4*)&lds[buf][1][(32 * i + row) * kPitch + piece] = xr[i];
+  auto issue_one = [&](const Target& t, int idx) {
+    if (idx < kLoads) load_to_lds16(t.w + woff[idx], t.lds + idx * 512);
+    else load_to_lds16(t.x + soff[idx - kLoads], t.lds + kStageElems + (idx - kLoads) * 512);
   };
 
   f32x16 acc[4][4];
@@ -142,34 +205,61 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-  auto compute = [&](int buf) {
-    const uint16_t* A = &lds[buf][0][(128 * wc + (lane & 31)) * kPitch + 32 * hh];
-    const uint16_t* B = &lds[buf][1][(128 * wt + (lane & 31)) * kPitch + 32 * hh];
+  // fragment reads: row R = (wave base) + 32 i + lane % 32 has swizzle(R) == swizzle(lane % 32); lane half hh
+  // covers logical pieces hh kSteps .. hh kSteps + kSteps - 1, k-step s takes piece hh kSteps + s
+  const int swz = swizzle<KC>(lane & 31);
+  int frag_off[kSteps];
 #pragma unroll
-    for (int s = 0; s < kKC / 16; ++s) {
-      bf16x8 a[4], b[4];
+  for (int st = 0; st < kSteps; ++st) frag_off[st] = 8 * ((hh * kSteps + st) ^ swz);
+  static_assert(2 * kLoads == 4 * kSteps, "one load per four MFMAs");
+  // One chunk from `stage`, with the loads of a later chunk (`nt`) issued one per four MFMAs (so
+  // no wave stalls on a burst of load issues before its first MFMA) and the next k-step's
+  // fragments read during the current one.  The order is pinned with scheduling barriers.
+  auto compute = [&](int stage, const Target& nt) {
+    const uint16_t* A = smem + stage * 2 * kStageElems + (128 * wc + (lane & 31)) * KC;
+    const uint16_t* B = smem + stage * 2 * kStageElems + kStageElems + (128 * wt + (lane & 31)) * KC;
+    bf16x8 a[2][4], b[2][4];
+    auto read = [&](int st, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = as_bf16x8(*(const u32x4*)(A + 32 * i * kPitch + 8 * s));
+      for (int i = 0; i < 4; ++i) fa[i] = as_bf16x8(*(const u32x4*)(A + 32 * i * KC + frag_off[st]));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = as_bf16x8(*(const u32x4*)(B + 32 * j * kPitch + 8 * s));
+      for (int j = 0; j < 4; ++j) fb[j] = as_bf16x8(*(const u32x4*)(B + 32 * j * KC + frag_off[st]));
+    };
+    read(0, a[0], b[0]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int st = 0; st < kSteps; ++st) {
+      if (st + 1 < kSteps) read(st + 1, a[(st + 1) & 1], b[(st + 1) & 1]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[st & 1][i], b[st & 1][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_one(nt, 4 * st + i);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
 
-  // ---- main loop: chunk c computes from buffer c & 1 while chunk c + 1 is loaded ----
-  gload(cbeg);
-  lstore(0);
-  __syncthreads();
-  for (int c = cbeg; c < cend; ++c) {
-    const int buf = (c - cbeg) & 1;
-    gload(c + 1 < cend ? c + 1 : c);    // the last refill re-reads its own chunk into the idle buffer
-    compute(buf);
-    lstore(buf ^ 1);
-    __syncthreads();
+  // ---- main loop.  Chunks 0 .. NS - 2 are issued up front; iteration c waits for chunk c (the
+  // NS - 2 younger chunks may stay in flight), passes a barrier (every wave is then done with
+  // chunk c - 1, so its stage is free) and computes c while issuing chunk c + NS - 1 into that
+  // stage.  Loads past the last chunk re-read it into a stage nobody reads again. ----
+#pragma unroll
+  for (int c = 0; c < NS - 1; ++c) {
+    const Target t = target(c < nch ? c : nch - 1, c);
+#pragma unroll
+    for (int idx = 0; idx < 2 * kLoads; ++idx) issue_one(t, idx);
   }
+  int stage = 0;
+  for (int c = 0; c < nch; ++c) {
+    wait_vmcnt<(NS - 2) * 2 * kLoads>();
+    lds_barrier();
+    const int nxt = c + NS - 1;
+    compute(stage, target(nxt < nch ? nxt : nch - 1, stage == 0 ? NS - 1 : stage - 1));
+    stage = stage == NS - 1 ? 0 : stage + 1;
+  }
+  wait_vmcnt<0>();     // the trailing re-reads land before the workgroup ends
 
   const int head = mt * 2 + wc;       // this wave's KV head
   if constexpr (SPLIT) {
@@ -190,59 +280,62 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
     }
     return;
   } else {
-    // RoPE (keys), bf16 rounding and a transpose into an LDS tile [token][channel] (the loop's
-    // last barrier freed the operand buffers).  Channel m = 32 i + 8 q + 4 hh + e of the head
-    // (i < 2) pairs with m + 64, held in block i + 2 of the same lane.
-    const bool rot = g == 0 && p.rope_keys;
-    uint16_t* O = &lds[0][0][0];
+    // RoPE (keys) and bf16 rounding in registers, then 8-byte stores straight into the page
+    // slots (L2 merges a row's sixteen 16-byte pieces): the lane of token column t and half hh
+    // holds channels 32 i + 8 q + 4 hh .. + 3 of its head in register quad q of block i, and
+    // channel m (i < 2) pairs with m + 64, held in block i + 2 of the same lane.
+    const int head = mt * 2 + wc;
+    if (head < p.hkv) {
+      uint16_t* dst = (g ? p.v_dst : p.k_dst) + (int64_t)head * p.dst_head_stride + 4 * hh;
+      // keys: the angle of channel pair m at position t is t theta^(-2m/128); in revolutions,
+      // t * rev[m] is formed in float64 and reduced to [0, 1) exactly enough that the
+      // hardware's sine and cosine of one revolution (v_sin_f32 / v_cos_f32) stay within
+      // 3e-7 of the float64 values -- far below a bf16 step of the output
+      auto emit = [&](int j, auto rot_t) {
+        constexpr bool kRot = decltype(rot_t)::value;
+        const int tl = 128 * wt + 32 * j + (lane & 31);
+        if (n0 + tl >= p.n_tokens) return;
+        uint16_t* row = dst + t_dst[tl];
+        const double pos = (double)t_pos[tl];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tl = 128 * wt + 32 * j + (lane & 31);
-      const float2* cs = p.rope + (int64_t)t_pos[tl] * kHalfDim;
-      uint16_t* orow = O + tl * kOutPitch + 128 * wc + 4 * hh;
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+          for (int q = 0; q < 4; ++q) {
+            float x1[4], x2[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int m = 32 * i + 8 * q + 4 * hh;
-          float x1[4], x2[4];
+            for (int e = 0; e < 4; ++e) {
+              x1[e] = acc[i][j][4 * q + e];
+              x2[e] = acc[i + 2][j][4 * q + e];
+            }
+            if constexpr (kRot) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            x1[e] = acc[i][j][4 * q + e];
-            x2[e] = acc[i + 2][j][4 * q + e];
+              for (int e = 0; e < 4; ++e) {
+                double r = pos * t_rev[32 * i + 8 * q + 4 * hh + e];
+                r -= floor(r);
+                const float u = (float)r;
+                const float c = __builtin_amdgcn_cosf(u), sn = __builtin_amdgcn_sinf(u);
+                const float y1 = x1[e] * c - x2[e] * sn;
+                const float y2 = x2[e] * c + x1[e] * sn;
+                x1[e] = y1;
+                x2[e] = y2;
+              }
+            }
+            u32x2 v1, v2;
+            v1[0] = pack_bf16x2(x1[0], x1[1]);
+            v1[1] = pack_bf16x2(x1[2], x1[3]);
+            v2[0] = pack_bf16x2(x2[0], x2[1]);
+            v2[1] = pack_bf16x2(x2[2], x2[3]);
+            *(u32x2*)(row + 32 * i + 8 * q) = v1;
+            *(u32x2*)(row + 64 + 32 * i + 8 * q) = v2;
           }
-          // branch-free: values take cos = 1, sin = 0, which leaves them exactly as they are
-          const float4 c01 = *(const float4*)(cs + m);
-          const float4 c23 = *(const float4*)(cs + m + 2);
-          const float cv[4] = {rot ? c01.x : 1.0f, rot ? c01.z : 1.0f, rot ? c23.x : 1.0f, rot ? c23.z : 1.0f};
-          const float sv[4] = {rot ? c01.y : 0.0f, rot ? c01.w : 0.0f, rot ? c23.y : 0.0f, rot ? c23.w : 0.0f};
+      };
+      if (g == 0 && p.rope_keys) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float y1 = x1[e] * cv[e] - x2[e] * sv[e];
-            const float y2 = x2[e] * cv[e] + x1[e] * sv[e];
-            x1[e] = y1;
-            x2[e] = y2;
-          }
-          u32x2 v1, v2;
-          v1[0] = pack_bf16x2(x1[0], x1[1]);
-          v1[1] = pack_bf16x2(x1[2], x1[3]);
-          v2[0] = pack_bf16x2(x2[0], x2[1]);
-          v2[1] = pack_bf16x2(x2[2], x2[3]);
-          *(u32x2*)(orow + 32 * i + 8 * q) = v1;
-          *(u32x2*)(orow + 64 + 32 * i + 8 * q) = v2;
-        }
-    }
-    __syncthreads();
-    // one (token, head) row is 16 pieces of 16 bytes; thread t stores pieces t, t + 256, ...
-    uint16_t* dst = g ? p.v_dst : p.k_dst;
-#pragma unroll 4
-    for (int it = 0; it < kProjTile * 2 * 16 / 256; ++it) {
-      const int id = it * 256 + tid;
-      const int tl = id >> 5, hd = (id >> 4) & 1, pc = (id & 15) * 8;
-      const int hx = mt * 2 + hd;
-      if (n0 + tl < p.n_tokens && hx < p.hkv)
-        *(u32x4*)(dst + t_dst[tl] + (int64_t)hx * p.dst_head_stride + pc) =
-            *(const u32x4*)(O + tl * kOutPitch + hd * kHeadDim + pc);
+        for (int j = 0; j < 4; ++j) emit(j, std::true_type{});
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) emit(j, std::false_type{});
+      }
     }
   }
 }
@@ -325,10 +418,11 @@ __global__ void fill_kernel(int32_t* flag, int32_t v) { *flag = v; }
 
 hipError_t launch_kvproj(const KvProjParams& p, hipStream_t s) {
   const int grid = (p.work_items + 7) / 8 * 8;
+  constexpr int KC = KVSHOT_KVPROJ_KC, NS = KVSHOT_KVPROJ_NS;
   if (p.splits > 1)
-    hipLaunchKernelGGL(kvproj_kernel<true>, dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((kvproj_kernel<true, KC, NS>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(kvproj_kernel<false>, dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((kvproj_kernel<false, KC, NS>), dim3(grid), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

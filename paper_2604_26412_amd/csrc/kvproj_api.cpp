@@ -27,6 +27,7 @@ struct kvshot_kvproj_ctx {
   kvshot_kvproj_config cfg;
   int device = 0, num_cus = 256, page_shift = 0;
   float2* rope = nullptr;
+  double* rope_rev = nullptr;
   float* part = nullptr;
   size_t ws_rows = 0;           // capacity of the partial workspace in (split, token) rows of 2 d_kv floats
   int32_t* flag = nullptr;
@@ -72,6 +73,7 @@ void free_proj(kvshot_kvproj_ctx* c) {
     for (auto& e : s.ev)
       if (e) (void)hipEventDestroy(e);
   if (c->rope) (void)hipFree(c->rope);
+  if (c->rope_rev) (void)hipFree(c->rope_rev);
   if (c->part) (void)hipFree(c->part);
   if (c->flag) (void)hipFree(c->flag);
   if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
@@ -115,6 +117,7 @@ kvshot_status base_params(const kvshot_kvproj_ctx* c, int32_t n_tokens, int32_t 
   p.token_seq = token_seq;
   p.token_pos = token_pos;
   p.rope = c->rope;
+  p.rope_rev = c->rope_rev;
   p.part = c->part;
   p.page_stride = g.page_stride;
   p.head_stride = g.head_stride;
@@ -192,14 +195,20 @@ kvshot_status kvshot_kvproj_init(const kvshot_kvproj_config* cfg, kvshot_kvproj_
       const double a = (double)pos * std::pow(g.rope_theta, -2.0 * m / (double)kHeadDim);
       tab[(size_t)pos * kHalfDim + m] = make_float2((float)std::cos(a), (float)std::sin(a));
     }
+  // the same angles in revolutions per position, for the fused kernel's own range reduction
+  double rev[kHalfDim];
+  for (int m = 0; m < kHalfDim; ++m)
+    rev[m] = std::pow(g.rope_theta, -2.0 * m / (double)kHeadDim) / (2.0 * 3.14159265358979323846);
   if (hipMalloc((void**)&c->rope, nrope * sizeof(float2)) != hipSuccess ||
+      hipMalloc((void**)&c->rope_rev, sizeof(rev)) != hipSuccess ||
       hipMalloc((void**)&c->part, c->ws_rows * 2 * d_kv * sizeof(float)) != hipSuccess ||
       hipMalloc((void**)&c->flag, sizeof(int32_t)) != hipSuccess) {
     (void)hipGetLastError();
     free_proj(c);
     return KVSHOT_ERR_OUT_OF_MEMORY;
   }
-  if (hipMemcpy(c->rope, tab.data(), nrope * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
+  if (hipMemcpy(c->rope, tab.data(), nrope * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->rope_rev, rev, sizeof(rev), hipMemcpyHostToDevice) != hipSuccess) {
     free_proj(c);
     return KVSHOT_ERR_DEVICE;
   }

@@ -27,6 +27,7 @@ struct KvProjParams {
   const int32_t* token_seq;                // [n_tokens]
   const int32_t* token_pos;
   const float2* rope;                      // [max_position][64] (cos, sin)
+  const double* rope_rev;                  // [64]: theta^(-2m/128) / (2 pi), revolutions per position
   float* part;                             // [splits][n_tokens][2 d_kv] (split plans only)
   int64_t page_stride, head_stride, slot_stride;
   int64_t dst_page_stride, dst_head_stride, dst_slot_stride;
