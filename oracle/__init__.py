@@ -43,6 +43,10 @@ Parity status per function:
     unit key, linearity, page-permutation invariance).  The stacking order
     and the rotation of the projected key at the token's position are
     readings: parity unpinned against the paper.
+  * ``metrics`` -- step-wise acceptance rates, retention and MAT (Sec. 3.1,
+    Metrics); pinned by the paper's complete acceptance-rate table (App. C),
+    the printed retention ratios and a telescoping identity.  Reading
+    conditional rates from accepted lengths is unpinned beyond that identity.
 """
 from .attention import (  # noqa: F401
     decode,
@@ -58,3 +62,4 @@ from .attention import (  # noqa: F401
 )
 from .fusion import gated_delta_fusion, sigmoid  # noqa: F401,E402
 from .kvproj import project_kv, scatter_tokens, stacked_layers  # noqa: F401,E402
+from .metrics import acceptance_counts, acceptance_rates, mat_from_alphas, retention  # noqa: F401,E402
