@@ -214,13 +214,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", choices=["attention", "fusion", "kvproj"], default="attention",
+    ap.add_argument("--op", choices=["attention", "fusion", "kvproj", "accept"], default="attention",
                     help="attention: the draft-step attention path (default); fusion: the hybrid drafter's "
-                         "gated delta fusion; kvproj: the projected-KV cache builder of KV-only drafters")
+                         "gated delta fusion; kvproj: the projected-KV cache builder of KV-only drafters; "
+                         "accept: acceptance rates and MAT over verification records")
     ap.add_argument("--workload", default=None,
                     choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8",
                              "fusion_t64_d4096", "fusion_t480_d4096", "kvproj_prefill_b64_t32k",
-                             "kvproj_verify_b64_t32k"])
+                             "kvproj_verify_b64_t32k", "accept_n64m_k7"])
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
@@ -250,6 +251,8 @@ def main():
         return bench_fusion(args, torch, K, W)
     if args.op == "kvproj":
         return bench_kvproj(args, torch, K, W)
+    if args.op == "accept":
+        return bench_accept(args, torch, K, W)
     if args.workload is None:
         args.workload = DEFAULT_WORKLOAD
     if args.workload.startswith("fusion"):
@@ -848,6 +851,116 @@ def bench_kvproj(args, torch, K, W):
         res["parity_sample"] = parity
     print(json.dumps(res), flush=True)
     proj.close()
+
+
+# ---------------------------------------------------------------------------
+# drafting metrics (--op accept)
+# ---------------------------------------------------------------------------
+
+ACCEPT_METRIC = "acceptance statistics (counts, step-wise rates, MAT) over verification records: records/s"
+
+
+def bench_accept(args, torch, K, W):
+    import numpy as np
+
+    name = args.workload or "accept_n64m_k7"
+    if name not in W.ACCEPT_WORKLOADS:
+        raise SystemExit(f"--op accept takes one of {sorted(W.ACCEPT_WORKLOADS)}")
+    spec = W.ACCEPT_WORKLOADS[name]
+    n, steps_k = spec["n"], spec["K"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(spec["seed"])
+    acc = torch.zeros((n,), dtype=torch.int32, device="cuda")
+    alive = torch.ones((n,), dtype=torch.bool, device="cuda")
+    for a in spec["rates"]:
+        alive &= torch.rand((n,), generator=g, device="cuda") < a
+        acc += alive.to(torch.int32)
+    del alive
+    torch.cuda.synchronize()
+    log(f"{name}: {n} records, K = {steps_k}")
+
+    counts = torch.empty((steps_k + 1,), dtype=torch.int64, device="cuda")
+    alpha = torch.empty((steps_k,), dtype=torch.float64, device="cuda")
+    mat = torch.empty((1,), dtype=torch.float64, device="cuda")
+    ret = torch.empty((1,), dtype=torch.float64, device="cuda")
+    lib = K.load_library()
+
+    def step():
+        st = lib.kvshot_acceptance_stats(acc.data_ptr(), n, steps_k, counts.data_ptr(), alpha.data_ptr(),
+                                         mat.data_ptr(), ret.data_ptr(), 6,
+                                         torch.cuda.current_stream().cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"kvshot_acceptance_stats failed: {st}")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    run_step = step
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        for _ in range(args.warmup):
+            run_step()
+        torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = 4 * n
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    log(f"step {ms:.4f} ms; MAT {float(mat.cpu()[0]):.4f}")
+    res = {
+        "metric": ACCEPT_METRIC,
+        "value": round(n / (ms * 1e-3), 1),
+        "unit": "records/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {n} accepted lengths (int32), K {steps_k}, a Markov chain with the "
+                               f"gated-KV (checkpoint) step-wise rates", "records": n, "K": steps_k,
+                   "launch": "python" if args.no_graph else "hip graph replay"},
+        # the three launches of one call (fill, histogram, finish) are timed together: the histogram's
+        # own share is at least this rate
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "packed_histogram_kernel (+ fill and finish launches, timed together)",
+                     "algorithmic_bytes_per_launch": nbytes},
+        "result": {"mat": float(mat.cpu()[0]), "retention": float(ret.cpu()[0]),
+                   "alpha": [round(float(x), 6) for x in alpha.cpu()]},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        host = acc.cpu().numpy()
+        t0 = time.perf_counter()
+        rc = oracle.acceptance_counts(host, steps_k)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "records/s", "cores": 1, "kind": "oracle",
+                               "host_cpus": os.cpu_count(), "seconds": round(dt, 3),
+                               "sample": f"all {n} records, NumPy counting (one thread)"}
+        res["parity_sample"] = {"counts_equal": bool(np.array_equal(rc, counts.cpu().numpy())),
+                                "mat_abs_diff": abs(float(mat.cpu()[0]) -
+                                                    oracle.mat_from_alphas(oracle.acceptance_rates(rc)))}
+    print(json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

@@ -13,8 +13,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["DraftAttention", "GatedDeltaFusion", "KvProjection", "KvshotError", "load_library", "LIB_PATH",
-           "EXPORTED_SYMBOLS"]
+__all__ = ["DraftAttention", "GatedDeltaFusion", "KvProjection", "KvshotError", "acceptance_stats", "load_library",
+           "LIB_PATH", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
@@ -34,6 +34,7 @@ EXPORTED_SYMBOLS = [
     "kvshot_gated_delta_fusion_packed",
     "kvshot_kvproj_init", "kvshot_kvproj_destroy", "kvshot_kv_project", "kvshot_kv_project_validate",
     "kvshot_kvproj_set_option", "kvshot_kvproj_plan", "kvshot_kvproj_profile_read",
+    "kvshot_acceptance_stats",
 ]
 FUSION_CROSS_ONLY, FUSION_OUT_FP32 = 1, 2
 KVPROJ_ROPE = 1
@@ -130,6 +131,7 @@ def load_library(path: Optional[str] = None):
         "kvshot_kvproj_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32)],
         "kvshot_kvproj_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_i64)],
+        "kvshot_acceptance_stats": [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i32, _vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -389,6 +391,26 @@ class DraftAttention:
             self._h, B, n, self._tensor(parents, "parents", torch.int32, (B, n)), anc.data_ptr(), depth.data_ptr(),
             self._stream(stream)))
         return anc, depth
+
+
+def acceptance_stats(accepted, K: int, retention_step: Optional[int] = None, stream=None):
+    """Counts c_k = #{a >= k} (int64 [K + 1]), step-wise rates alpha (float64 [K]), MAT (float64 [1]) and,
+    with ``retention_step``, alpha[retention_step] / alpha[0] (float64 [1]) for the accepted draft lengths
+    ``accepted`` (int32 device tensor) -- C ABI in ``include/kvshot_metrics.h``."""
+    torch = _torch()
+    lib = load_library()
+    dev = accepted.device
+    n = accepted.numel()
+    acc = GatedDeltaFusion._tensor(accepted, "accepted", torch.int32, (n,)) if n else None
+    counts = torch.empty((K + 1,), dtype=torch.int64, device=dev)
+    alpha = torch.empty((K,), dtype=torch.float64, device=dev)
+    mat = torch.empty((1,), dtype=torch.float64, device=dev)
+    ret = torch.empty((1,), dtype=torch.float64, device=dev) if retention_step is not None else None
+    _check("kvshot_acceptance_stats", lib.kvshot_acceptance_stats(
+        acc, n, K, counts.data_ptr(), alpha.data_ptr(), mat.data_ptr(), ret.data_ptr() if ret is not None else None,
+        retention_step if retention_step is not None else 0,
+        stream if stream is not None else torch.cuda.current_stream().cuda_stream))
+    return counts, alpha, mat, ret
 
 
 class GatedDeltaFusion:

@@ -203,3 +203,15 @@ def test_kvproj_config_struct_layout_matches_the_header():
     body = text[text.index("typedef struct kvshot_kvproj_config {"):text.index("} kvshot_kvproj_config;")]
     fields = re.findall(r"^\s*[a-z0-9_]+\s+([a-z_0-9]+);", body, flags=re.M)
     assert fields == [f for f, _ in K.KvprojConfig._fields_]
+
+
+def test_acceptance_stats_rejects_bad_arguments_before_any_device_call(lib):
+    f = lib.kvshot_acceptance_stats
+    ok = ctypes.c_void_p(64)    # aligned, never dereferenced: every case below fails on the host
+    assert f(None, -1, 7, ok, ok, ok, None, 0, None) == 1
+    assert f(None, 5, 7, ok, ok, ok, None, 0, None) == 1          # records missing
+    assert f(ok, 5, 0, ok, ok, ok, None, 0, None) == 1            # K out of range
+    assert f(ok, 5, 256, ok, ok, ok, None, 0, None) == 1
+    assert f(ok, 5, 7, None, ok, ok, None, 0, None) == 1
+    assert f(ok, 5, 7, ok, ok, ok, ok, 7, None) == 1              # retention step past K - 1
+    assert f(ctypes.c_void_p(66), 5, 7, ok, ok, ok, None, 0, None) == 1   # misaligned

@@ -469,3 +469,18 @@ def kvproj_algorithmic(n_tokens: int, layers: int = 3, d_kv: int = 1024) -> dict
     out = 2 * n_tokens * d_kv * 2
     flops = 2 * 2 * n_tokens * d_kv * layers * d_kv
     return dict(bytes=src + weights + out, flops=flops, src=src, weights=weights, out=out)
+
+
+# ---------------------------------------------------------------------------
+# drafting metrics: per-verification accepted draft lengths
+# ---------------------------------------------------------------------------
+
+# Step-wise acceptance rates alpha_0 .. alpha_6 of the 1-layer gated KV drafter
+# initialised from a checkpoint (App. C, table of complete step-wise rates).
+GATED_KV_CKPT_RATES = (0.665, 0.603, 0.573, 0.553, 0.537, 0.525, 0.514)
+
+ACCEPT_WORKLOADS = {
+    # 64M verification records (one per sequence and verification), K = 7 draft steps: each
+    # step accepted with probability alpha_k while the earlier ones were
+    "accept_n64m_k7": dict(n=1 << 26, K=7, rates=GATED_KV_CKPT_RATES, seed=4101),
+}
