@@ -47,6 +47,12 @@ Parity status per function:
     Metrics); pinned by the paper's complete acceptance-rate table (App. C),
     the printed retention ratios and a telescoping identity.  Reading
     conditional rates from accepted lengths is unpinned beyond that identity.
+  * ``tree_grow`` -- level-wise growth of the (8, 10, 60) draft tree (Sec.
+    3.5): row-wise top-k with log-softmax, best-first frontier selection,
+    final selection of the n best nodes.  The selection rule is a reading
+    (the paper gives the shape only): parity unpinned against the paper;
+    pinned by a plain scan, a closed-form two-token example, the greedy
+    chain at k = 1 and closure / order / optimality invariants.
 """
 from .attention import (  # noqa: F401
     decode,
@@ -63,3 +69,4 @@ from .attention import (  # noqa: F401
 from .fusion import gated_delta_fusion, sigmoid  # noqa: F401,E402
 from .kvproj import project_kv, scatter_tokens, stacked_layers  # noqa: F401,E402
 from .metrics import acceptance_counts, acceptance_rates, mat_from_alphas, retention  # noqa: F401,E402
+from .tree_grow import finalize as tree_finalize, grow_level, grow_tree, log_softmax_topk  # noqa: F401,E402
