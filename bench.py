@@ -139,6 +139,20 @@ def call_bytes(d, n_q, draft_seen):
     return kv + pt + q + dkv + q
 
 
+def copy_calibration(torch, gib: float):
+    """One plain device copy of `gib` GiB: the reference a profiler's byte counters are scaled by."""
+    if gib <= 0:
+        return
+    nbytes = int(gib * (1 << 30))
+    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
+    del src, dst
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -214,14 +228,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", choices=["attention", "fusion", "kvproj", "accept"], default="attention",
+    ap.add_argument("--op", choices=["attention", "fusion", "kvproj", "accept", "treegrow"], default="attention",
                     help="attention: the draft-step attention path (default); fusion: the hybrid drafter's "
                          "gated delta fusion; kvproj: the projected-KV cache builder of KV-only drafters; "
-                         "accept: acceptance rates and MAT over verification records")
+                         "accept: acceptance rates and MAT over verification records; treegrow: level-wise "
+                         "draft-tree growth from the drafter's logits")
     ap.add_argument("--workload", default=None,
                     choices=[DEFAULT_WORKLOAD, "tree_b8_ctx16k_n60", "ragged_b16_k6", "single_ctx4096_k8",
                              "fusion_t64_d4096", "fusion_t480_d4096", "kvproj_prefill_b64_t32k",
-                             "kvproj_verify_b64_t32k", "accept_n64m_k7"])
+                             "kvproj_verify_b64_t32k", "accept_n64m_k7", "treegrow_b8_v152k_d8k10n60"])
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
@@ -253,6 +268,8 @@ def main():
         return bench_kvproj(args, torch, K, W)
     if args.op == "accept":
         return bench_accept(args, torch, K, W)
+    if args.op == "treegrow":
+        return bench_treegrow(args, torch, K, W)
     if args.workload is None:
         args.workload = DEFAULT_WORKLOAD
     if args.workload.startswith("fusion"):
@@ -304,15 +321,7 @@ def main():
     out_bytes = B * nq_call * Hq * D * (2 if d["dtype"] == "bf16" else 4)
     attn_launch_bytes = call_bytes(d, nq_call, draft_seen[-1]) - (out_bytes if plan["splits"] > 1 else 0)
 
-    if args.copy_calib_gib > 0:
-        nbytes = int(args.copy_calib_gib * (1 << 30))
-        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
-        del src, dst
+    copy_calibration(torch, args.copy_calib_gib)
 
     log(f"plan {plan}; warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -504,15 +513,7 @@ def bench_fusion(args, torch, K, W):
         else:
             fz(n, o, None, b_g, None, out=h, packed=packed)
 
-    if args.copy_calib_gib > 0:
-        nbytes = int(args.copy_calib_gib * (1 << 30))
-        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
-        del src, dst
+    copy_calibration(torch, args.copy_calib_gib)
 
     log(f"plan {plan}; warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -754,15 +755,7 @@ def bench_kvproj(args, torch, K, W):
         proj(d["k_src"], d["v_src"], d["table"], d["seq"], d["pos"], d["w_k"], d["w_v"], d["k_dst"], d["v_dst"],
              rope=rope)
 
-    if args.copy_calib_gib > 0:
-        nbytes = int(args.copy_calib_gib * (1 << 30))
-        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"copy calibration: {nbytes} bytes read and written by one copy kernel")
-        del src, dst
+    copy_calibration(torch, args.copy_calib_gib)
 
     log(f"{n} tokens; plan {plan}; warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -962,6 +955,152 @@ def bench_accept(args, torch, K, W):
                                                     oracle.mat_from_alphas(oracle.acceptance_rates(rc)))}
     print(json.dumps(res), flush=True)
 
+
+# ---------------------------------------------------------------------------
+# draft-tree growth (--op treegrow)
+# ---------------------------------------------------------------------------
+
+TREEGROW_METRIC = "level-wise draft-tree growth (depth 8, top-k 10, 60 nodes) from bf16 logits: trees/s"
+
+
+def capture(torch, fn):
+    """A HIP graph of fn() (one eager run on a side stream first, as torch asks)."""
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        fn()
+    torch.cuda.synchronize()
+    return graph
+
+
+def timed(torch, fn, steps):
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def bench_treegrow(args, torch, K, W):
+    import numpy as np
+
+    name = args.workload or "treegrow_b8_v152k_d8k10n60"
+    if name not in W.TREEGROW_WORKLOADS:
+        raise SystemExit(f"--op treegrow takes one of {sorted(W.TREEGROW_WORKLOADS)}")
+    spec = W.TREEGROW_WORKLOADS[name]
+    B, V, depth, k, n = spec["batch"], spec["vocab"], spec["depth"], spec["k"], spec["n"]
+    log(f"{name}: generating {depth} levels of logits")
+    host = W.treegrow_levels(spec)
+    levels = [torch.from_numpy(np.ascontiguousarray(h).view(np.int16)).view(torch.bfloat16).cuda() for h in host]
+    alg = W.treegrow_algorithmic(spec)
+    lib = K.load_library()
+    rows = [B * (1 if d == 0 else k) for d in range(depth)]
+    ws = torch.empty(max(K.topk_workspace_bytes(r, V) for r in rows), dtype=torch.uint8, device="cuda")
+    top_tok = [torch.empty((r, k), dtype=torch.int32, device="cuda") for r in rows]
+    top_lp = [torch.empty((r, k), dtype=torch.float32, device="cuda") for r in rows]
+    lpar = torch.empty((depth, B, k), dtype=torch.int32, device="cuda")
+    ltok = torch.empty((depth, B, k), dtype=torch.int32, device="cuda")
+    lsc = torch.empty((depth, B, k), dtype=torch.float32, device="cuda")
+    root = torch.zeros((B, 1), dtype=torch.float32, device="cuda")
+    out = [torch.empty((B, n), dtype=dt, device="cuda")
+           for dt in (torch.int32, torch.int32, torch.int32, torch.float32)]
+
+    def topk(d):
+        st = lib.kvshot_topk_logprobs(levels[d].data_ptr(), K.BF16, rows[d], V, V, k, top_tok[d].data_ptr(),
+                                      top_lp[d].data_ptr(), ws.data_ptr(), ws.numel(),
+                                      torch.cuda.current_stream().cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"kvshot_topk_logprobs failed: {st}")
+
+    def step():
+        s = torch.cuda.current_stream().cuda_stream
+        for d in range(depth):
+            topk(d)
+            F = 1 if d == 0 else k
+            sc = root if d == 0 else lsc[d - 1]
+            st = lib.kvshot_tree_expand(B, F, k, k, sc.data_ptr(), top_tok[d].data_ptr(), top_lp[d].data_ptr(),
+                                        lpar[d].data_ptr(), ltok[d].data_ptr(), lsc[d].data_ptr(), s)
+            if st != 0:
+                raise RuntimeError(f"kvshot_tree_expand failed: {st}")
+        st = lib.kvshot_tree_select(B, depth, k, n, lpar.data_ptr(), ltok.data_ptr(), lsc.data_ptr(),
+                                    *[o.data_ptr() for o in out], s)
+        if st != 0:
+            raise RuntimeError(f"kvshot_tree_select failed: {st}")
+
+    copy_calibration(torch, args.copy_calib_gib)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    run_step = step
+    if not args.no_graph:
+        run_step = capture(torch, step).replay
+        for _ in range(args.warmup):
+            run_step()
+    ms = timed(torch, run_step, args.steps)
+
+    # the dominant kernel: top-k of one 80-row level, 20 calls in one graph (chunk kernel + merge)
+    reps = 20
+    lvl = 1 if depth > 1 else 0
+    g_top = capture(torch, lambda: [topk(lvl) for _ in range(reps)])
+    g_top.replay()
+    top_ms = timed(torch, g_top.replay, max(5, args.steps // 5)) / reps
+    top_bytes = rows[lvl] * V * 2 + rows[lvl] * k * 8
+    achieved = top_bytes / (top_ms * 1e-3) / 1e9
+    step_gbs = alg["bytes"] / (ms * 1e-3) / 1e9
+    log(f"step {ms * 1e3:.1f} us ({step_gbs:.0f} GB/s over all levels); top-k of {rows[lvl]} rows "
+        f"{top_ms * 1e3:.2f} us = {achieved:.0f} GB/s")
+
+    res = {
+        "metric": TREEGROW_METRIC,
+        "value": round(B / (ms * 1e-3), 1),
+        "unit": "trees/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 logits, f32 scores",
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {B} sequences, vocabulary {V}, depth {depth}, top-k {k}, {n} nodes; "
+                               f"{alg['rows']} logit rows ({alg['logits'] / 1e6:.1f} MB) per tree batch",
+                   "batch": B, "vocab": V, "depth": depth, "k": k, "n": n,
+                   "launch": "python" if args.no_graph else "hip graph replay",
+                   "step_effective_gbs": round(step_gbs, 1)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": f"topk_chunk_kernel + topk_merge_kernel on one level of {rows[lvl]} rows "
+                               f"(timed together)",
+                     "algorithmic_bytes_per_launch": top_bytes},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        got = [o.cpu().numpy() for o in out]
+        t0 = time.perf_counter()
+        done, same = 0, 0
+        while done < B and (done == 0 or time.perf_counter() - t0 < 12.0):
+            lv = [W.bf16_bits_to_f32(h[done]).astype(np.float64) for h in host]
+            rp, rt, rd, rs = oracle.grow_tree(lv, k, n)
+            same += int(np.array_equal(rp, got[0][done]) and np.array_equal(rt, got[1][done]) and
+                        np.array_equal(rd, got[2][done]))
+            done += 1
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(done / dt, 4), "unit": "trees/s", "cores": 1,
+                               "kind": "oracle", "host_cpus": os.cpu_count(), "seconds": round(dt, 3),
+                               "sample": f"{done} of the {B} sequences' trees, float64 NumPy oracle (sorts "
+                                         f"run on one thread)"}
+        res["parity_sample"] = {"trees_checked": done, "trees_identical": same}
+    print(json.dumps(res), flush=True)
 
 if __name__ == "__main__":
     main()

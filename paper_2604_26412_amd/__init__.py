@@ -13,8 +13,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["DraftAttention", "GatedDeltaFusion", "KvProjection", "KvshotError", "acceptance_stats", "load_library",
-           "LIB_PATH", "EXPORTED_SYMBOLS"]
+__all__ = ["DraftAttention", "GatedDeltaFusion", "KvProjection", "KvshotError", "acceptance_stats", "topk_logprobs",
+           "tree_expand", "tree_select", "grow_tree", "load_library", "LIB_PATH", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
@@ -34,7 +34,7 @@ EXPORTED_SYMBOLS = [
     "kvshot_gated_delta_fusion_packed",
     "kvshot_kvproj_init", "kvshot_kvproj_destroy", "kvshot_kv_project", "kvshot_kv_project_validate",
     "kvshot_kvproj_set_option", "kvshot_kvproj_plan", "kvshot_kvproj_profile_read",
-    "kvshot_acceptance_stats",
+    "kvshot_acceptance_stats", "kvshot_topk_workspace_bytes", "kvshot_topk_logprobs", "kvshot_tree_expand", "kvshot_tree_select",
 ]
 FUSION_CROSS_ONLY, FUSION_OUT_FP32 = 1, 2
 KVPROJ_ROPE = 1
@@ -132,11 +132,16 @@ def load_library(path: Optional[str] = None):
         "kvshot_kvproj_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_i64)],
         "kvshot_acceptance_stats": [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i32, _vp],
+        "kvshot_topk_logprobs": [_vp, _i32, _i32, _i32, _i64, _i32, _vp, _vp, _vp, _i64, _vp],
+        "kvshot_tree_expand": [_i32, _i32, _i32, _i32] + [_vp] * 6 + [_vp],
+        "kvshot_tree_select": [_i32, _i32, _i32, _i32] + [_vp] * 7 + [_vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.kvshot_topk_workspace_bytes.argtypes = [_i32, _i32]
+    lib.kvshot_topk_workspace_bytes.restype = _i64
     lib.kvshot_status_string.argtypes = [_i32]
     lib.kvshot_status_string.restype = ctypes.c_char_p
     if path is None:
@@ -411,6 +416,103 @@ def acceptance_stats(accepted, K: int, retention_step: Optional[int] = None, str
         retention_step if retention_step is not None else 0,
         stream if stream is not None else torch.cuda.current_stream().cuda_stream))
     return counts, alpha, mat, ret
+
+
+def _stream_of(stream):
+    return stream if stream is not None else _torch().cuda.current_stream().cuda_stream
+
+
+def topk_workspace_bytes(rows: int, vocab: int) -> int:
+    """Device scratch ``topk_logprobs`` needs for ``rows`` rows of ``vocab`` logits (0: none)."""
+    n = load_library().kvshot_topk_workspace_bytes(int(rows), int(vocab))
+    if n < 0:
+        raise ValueError(f"no top-k plan for rows={rows}, vocab={vocab}")
+    return int(n)
+
+
+def topk_logprobs(logits, k: int, workspace=None, stream=None):
+    """Top-k tokens (int32 [..., k]) and their log-softmax values (float32 [..., k]) of each row of
+    ``logits`` (bf16 or float32 device tensor [..., vocab], rows contiguous) -- ``include/kvshot_tree.h``.
+    ``workspace``: a device tensor of at least ``topk_workspace_bytes`` bytes, allocated here if None."""
+    torch = _torch()
+    lib = load_library()
+    if logits.dtype not in (torch.bfloat16, torch.float32) or not logits.is_cuda or logits.stride(-1) != 1:
+        raise ValueError("logits must be a bf16 or float32 device tensor with contiguous rows")
+    vocab = logits.shape[-1]
+    rows = logits.numel() // vocab
+    flat = logits if logits.dim() == 2 else logits.reshape(rows, vocab)   # a 2-D view keeps its row stride
+    need = topk_workspace_bytes(rows, vocab)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    tokens = torch.empty(logits.shape[:-1] + (k,), dtype=torch.int32, device=logits.device)
+    lp = torch.empty(logits.shape[:-1] + (k,), dtype=torch.float32, device=logits.device)
+    _check("kvshot_topk_logprobs", lib.kvshot_topk_logprobs(
+        flat.data_ptr(), BF16 if logits.dtype == torch.bfloat16 else FP32, rows, vocab, flat.stride(0), k,
+        tokens.data_ptr(), lp.data_ptr(), ws_ptr, ws_bytes, _stream_of(stream)))
+    return tokens, lp
+
+
+def tree_expand(scores, tokens, logprobs, k: int, out=None, stream=None):
+    """Next frontier (parent index, token, score; each [batch][k]) from the frontier's scores [batch][F] and
+    proposals tokens / logprobs [batch][F][P]; ``out`` = (parent, token, score) buffers to fill."""
+    torch = _torch()
+    lib = load_library()
+    batch, frontier, proposals = tokens.shape
+    sc = GatedDeltaFusion._tensor(scores, "scores", torch.float32, (batch, frontier))
+    tk = GatedDeltaFusion._tensor(tokens, "tokens", torch.int32, (batch, frontier, proposals))
+    lp = GatedDeltaFusion._tensor(logprobs, "logprobs", torch.float32, (batch, frontier, proposals))
+    if out is None:
+        out = (torch.empty((batch, k), dtype=torch.int32, device=tokens.device),
+               torch.empty((batch, k), dtype=torch.int32, device=tokens.device),
+               torch.empty((batch, k), dtype=torch.float32, device=tokens.device))
+    par, tok, nsc = out
+    for t, name, dt in ((par, "parent", torch.int32), (tok, "token", torch.int32), (nsc, "score", torch.float32)):
+        GatedDeltaFusion._tensor(t, name, dt, (batch, k))
+    _check("kvshot_tree_expand", lib.kvshot_tree_expand(batch, frontier, proposals, k, sc, tk, lp, par.data_ptr(),
+                                                        tok.data_ptr(), nsc.data_ptr(), _stream_of(stream)))
+    return par, tok, nsc
+
+
+def tree_select(level_parent, level_tokens, level_scores, n: int, stream=None):
+    """The tree (parents, tokens, depths, scores; each [batch][n]) from the frontiers of every level
+    ([depth][batch][k] each)."""
+    torch = _torch()
+    lib = load_library()
+    depth, batch, k = level_tokens.shape
+    lpar = GatedDeltaFusion._tensor(level_parent, "level_parent", torch.int32, (depth, batch, k))
+    ltok = GatedDeltaFusion._tensor(level_tokens, "level_tokens", torch.int32, (depth, batch, k))
+    lsc = GatedDeltaFusion._tensor(level_scores, "level_scores", torch.float32, (depth, batch, k))
+    dev = level_tokens.device
+    out = [torch.empty((batch, n), dtype=torch.int32, device=dev) for _ in range(3)]
+    osc = torch.empty((batch, n), dtype=torch.float32, device=dev)
+    _check("kvshot_tree_select", lib.kvshot_tree_select(batch, depth, k, n, lpar, ltok, lsc, out[0].data_ptr(),
+                                                        out[1].data_ptr(), out[2].data_ptr(), osc.data_ptr(),
+                                                        _stream_of(stream)))
+    return out[0], out[1], out[2], osc
+
+
+def grow_tree(level_logits, k: int, n: int, stream=None):
+    """Grow a tree level by level: ``level_logits[d]`` holds the drafter's logits for level d's frontier
+    ([batch][1][vocab] for the root, then [batch][k][vocab], frontier nodes in the order the previous level
+    returned them).  Only sequences the library calls."""
+    torch = _torch()
+    batch = level_logits[0].shape[0]
+    dev = level_logits[0].device
+    depth = len(level_logits)
+    lpar = torch.empty((depth, batch, k), dtype=torch.int32, device=dev)
+    ltok = torch.empty((depth, batch, k), dtype=torch.int32, device=dev)
+    lsc = torch.empty((depth, batch, k), dtype=torch.float32, device=dev)
+    scores = torch.zeros((batch, 1), dtype=torch.float32, device=dev)
+    vocab = level_logits[0].shape[-1]
+    need = max(topk_workspace_bytes(z.numel() // vocab, vocab) for z in level_logits)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    for d, z in enumerate(level_logits):
+        tok, lp = topk_logprobs(z, k, workspace=ws, stream=stream)
+        tree_expand(scores, tok, lp, k, out=(lpar[d], ltok[d], lsc[d]), stream=stream)
+        scores = lsc[d]
+    return tree_select(lpar, ltok, lsc, n, stream)
 
 
 class GatedDeltaFusion:

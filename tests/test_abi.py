@@ -215,3 +215,40 @@ def test_acceptance_stats_rejects_bad_arguments_before_any_device_call(lib):
     assert f(ok, 5, 7, None, ok, ok, None, 0, None) == 1
     assert f(ok, 5, 7, ok, ok, ok, ok, 7, None) == 1              # retention step past K - 1
     assert f(ctypes.c_void_p(66), 5, 7, ok, ok, ok, None, 0, None) == 1   # misaligned
+
+
+def test_topk_workspace_sizes(lib):
+    f = lib.kvshot_topk_workspace_bytes
+    assert f(80, 16384) == 0                       # one chunk: finished in place
+    assert f(80, 16385) == 80 * 2 * 136
+    assert f(80, 151936) == 80 * 10 * 136
+    assert f(1, 64 * 16384) == 64 * 136
+    assert f(1, 64 * 16384 + 1) == -1 and f(0, 100) == -1 and f(3, 0) == -1
+
+
+def test_tree_calls_reject_bad_arguments_before_any_device_call(lib):
+    ok = ctypes.c_void_p(256)   # aligned, never dereferenced: every case below fails on the host
+    top = lib.kvshot_topk_logprobs
+    assert top(ok, 0, 4, 100, 104, 17, ok, ok, None, 0, None) == 1        # k > 16
+    assert top(ok, 0, 4, 100, 104, 0, ok, ok, None, 0, None) == 1
+    assert top(ok, 0, 4, 5, 8, 6, ok, ok, None, 0, None) == 1             # k > vocab
+    assert top(ok, 1, 4, 100, 99, 4, ok, ok, None, 0, None) == 1          # stride < vocab
+    assert top(ctypes.c_void_p(257), 0, 4, 100, 104, 4, ok, ok, None, 0, None) == 1   # bf16 not 2-byte aligned
+    assert top(ctypes.c_void_p(258), 1, 4, 100, 104, 4, ok, ok, None, 0, None) == 1   # float32 not 4-byte aligned
+    assert top(ok, 7, 4, 100, 104, 4, ok, ok, None, 0, None) == 1         # dtype
+    assert top(ok, 0, 4, 20000, 20000, 4, ok, ok, None, 0, None) == 1     # workspace missing
+    need = lib.kvshot_topk_workspace_bytes(4, 20000)
+    assert top(ok, 0, 4, 20000, 20000, 4, ok, ok, ok, need - 1, None) == 1
+    assert top(None, 0, 4, 100, 104, 4, ok, ok, None, 0, None) == 1
+    ex = lib.kvshot_tree_expand
+    assert ex(2, 17, 10, 10, ok, ok, ok, ok, ok, ok, None) == 1           # frontier > 16
+    assert ex(2, 10, 17, 10, ok, ok, ok, ok, ok, ok, None) == 1
+    assert ex(2, 1, 4, 5, ok, ok, ok, ok, ok, ok, None) == 1              # k > frontier * proposals
+    assert ex(2, 10, 10, 17, ok, ok, ok, ok, ok, ok, None) == 1
+    assert ex(0, 10, 10, 10, ok, ok, ok, ok, ok, ok, None) == 1
+    assert ex(2, 10, 10, 10, ok, ok, None, ok, ok, ok, None) == 1
+    sel = lib.kvshot_tree_select
+    assert sel(2, 17, 16, 60, ok, ok, ok, ok, ok, ok, ok, None) == 1      # depth * k > 256
+    assert sel(2, 8, 10, 81, ok, ok, ok, ok, ok, ok, ok, None) == 1       # n > depth * k
+    assert sel(2, 8, 10, 0, ok, ok, ok, ok, ok, ok, ok, None) == 1
+    assert sel(2, 8, 10, 60, ok, ok, ok, ok, ok, None, ok, None) == 1

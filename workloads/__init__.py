@@ -43,6 +43,8 @@ _TID_PERM = 4
 _TID_LENS = 5
 _TID_OFFS = 6
 _TID_OUTLIER = 7
+_TID_LOGITS = 8
+_TID_PEAKS = 9
 _TID_K = 1000   # + b
 _TID_V = 2000   # + b
 _TID_TREE = 3000  # + b
@@ -484,3 +486,51 @@ ACCEPT_WORKLOADS = {
     # step accepted with probability alpha_k while the earlier ones were
     "accept_n64m_k7": dict(n=1 << 26, K=7, rates=GATED_KV_CKPT_RATES, seed=4101),
 }
+
+
+# ---------------------------------------------------------------------------
+# draft-tree growth: drafter logits over the vocabulary
+# ---------------------------------------------------------------------------
+
+def draft_logits(seed: int, rows: int, vocab: int, *, dtype: str = "bf16", sigma: float = 2.0, peaks: int = 8,
+                 peak_max: float = 12.0, grid: float = None, stream: int = 0) -> np.ndarray:
+    """Seeded synthetic drafter logits [rows][vocab]: a sigma * N(0, 1) background with `peaks` random
+    tokens per row raised by U(0, peak_max) -- a peaked next-token distribution whose top tokens carry
+    most of the mass.  ``grid`` rounds every logit to a multiple of it (many equal logits); ``stream``
+    selects an independent draw for the same seed (one per tree level)."""
+    x = _normal(seed, _TID_LOGITS + 1000 * stream, (rows, vocab)) * np.float32(sigma)
+    if peaks:
+        g = rng_for(seed, _TID_PEAKS + 1000 * stream)
+        idx = g.integers(0, vocab, size=(rows, peaks))
+        x[np.arange(rows)[:, None], idx] += g.uniform(0.0, peak_max, size=(rows, peaks)).astype(np.float32)
+    if grid:
+        x = np.round(x / np.float32(grid)) * np.float32(grid)
+    return _encode(x.astype(np.float32), dtype)
+
+
+TREEGROW_WORKLOADS = {
+    # tree (8, 10, 60) of Sec. 3.5 for a batch of 8 sequences over Qwen3-8B's vocabulary: level 0
+    # expands the root (8 rows), levels 1..7 the 10-node frontiers (80 rows each), bf16 logits
+    "treegrow_b8_v152k_d8k10n60": dict(batch=8, vocab=151936, depth=8, k=10, n=60, dtype="bf16", seed=5101),
+}
+
+
+def treegrow_levels(spec: dict, *, vocab: int = None, batch: int = None):
+    """Per level d the logits [batch][F_d][vocab] (F_0 = 1, else k) of a tree-growth workload."""
+    V = vocab or spec["vocab"]
+    B = batch or spec["batch"]
+    out = []
+    for d in range(spec["depth"]):
+        F = 1 if d == 0 else spec["k"]
+        out.append(draft_logits(spec["seed"], B * F, V, dtype=spec["dtype"], stream=d).reshape(B, F, V))
+    return out
+
+
+def treegrow_algorithmic(spec: dict) -> dict:
+    """Bytes one growth step must move: every level's logits once, plus the level outputs."""
+    B, V, depth, k, n = spec["batch"], spec["vocab"], spec["depth"], spec["k"], spec["n"]
+    eb = 2 if spec["dtype"] == "bf16" else 4
+    rows = B * (1 + (depth - 1) * k)
+    logits = rows * V * eb
+    small = rows * k * 8 + depth * B * k * 12 + B * n * 16
+    return dict(bytes=logits + small, logits=logits, rows=rows)
