@@ -1004,9 +1004,7 @@ def bench_treegrow(args, torch, K, W):
     alg = W.treegrow_algorithmic(spec)
     lib = K.load_library()
     rows = [B * (1 if d == 0 else k) for d in range(depth)]
-    ws = torch.empty(max(K.topk_workspace_bytes(r, V) for r in rows), dtype=torch.uint8, device="cuda")
-    top_tok = [torch.empty((r, k), dtype=torch.int32, device="cuda") for r in rows]
-    top_lp = [torch.empty((r, k), dtype=torch.float32, device="cuda") for r in rows]
+    ws = K.tree_level_workspace(B, k, V)
     lpar = torch.empty((depth, B, k), dtype=torch.int32, device="cuda")
     ltok = torch.empty((depth, B, k), dtype=torch.int32, device="cuda")
     lsc = torch.empty((depth, B, k), dtype=torch.float32, device="cuda")
@@ -1014,25 +1012,20 @@ def bench_treegrow(args, torch, K, W):
     out = [torch.empty((B, n), dtype=dt, device="cuda")
            for dt in (torch.int32, torch.int32, torch.int32, torch.float32)]
 
-    def topk(d):
-        st = lib.kvshot_topk_logprobs(levels[d].data_ptr(), K.BF16, rows[d], V, V, k, top_tok[d].data_ptr(),
-                                      top_lp[d].data_ptr(), ws.data_ptr(), ws.numel(),
-                                      torch.cuda.current_stream().cuda_stream)
+    def level(d):
+        F = 1 if d == 0 else k
+        sc = root if d == 0 else lsc[d - 1]
+        st = lib.kvshot_tree_level(levels[d].data_ptr(), K.BF16, B, F, V, V, k, sc.data_ptr(), lpar[d].data_ptr(),
+                                   ltok[d].data_ptr(), lsc[d].data_ptr(), ws.data_ptr(), ws.numel(),
+                                   torch.cuda.current_stream().cuda_stream)
         if st != 0:
-            raise RuntimeError(f"kvshot_topk_logprobs failed: {st}")
+            raise RuntimeError(f"kvshot_tree_level failed: {st}")
 
     def step():
-        s = torch.cuda.current_stream().cuda_stream
         for d in range(depth):
-            topk(d)
-            F = 1 if d == 0 else k
-            sc = root if d == 0 else lsc[d - 1]
-            st = lib.kvshot_tree_expand(B, F, k, k, sc.data_ptr(), top_tok[d].data_ptr(), top_lp[d].data_ptr(),
-                                        lpar[d].data_ptr(), ltok[d].data_ptr(), lsc[d].data_ptr(), s)
-            if st != 0:
-                raise RuntimeError(f"kvshot_tree_expand failed: {st}")
+            level(d)
         st = lib.kvshot_tree_select(B, depth, k, n, lpar.data_ptr(), ltok.data_ptr(), lsc.data_ptr(),
-                                    *[o.data_ptr() for o in out], s)
+                                    *[o.data_ptr() for o in out], torch.cuda.current_stream().cuda_stream)
         if st != 0:
             raise RuntimeError(f"kvshot_tree_select failed: {st}")
 
@@ -1047,16 +1040,17 @@ def bench_treegrow(args, torch, K, W):
             run_step()
     ms = timed(torch, run_step, args.steps)
 
-    # the dominant kernel: top-k of one 80-row level, 20 calls in one graph (chunk kernel + merge)
+    # the dominant kernel: one 80-row level (chunk workgroups, the last of each sequence merging and
+    # expanding), 20 launches in one graph
     reps = 20
     lvl = 1 if depth > 1 else 0
-    g_top = capture(torch, lambda: [topk(lvl) for _ in range(reps)])
-    g_top.replay()
-    top_ms = timed(torch, g_top.replay, max(5, args.steps // 5)) / reps
-    top_bytes = rows[lvl] * V * 2 + rows[lvl] * k * 8
+    g_lvl = capture(torch, lambda: [level(lvl) for _ in range(reps)])
+    g_lvl.replay()
+    top_ms = timed(torch, g_lvl.replay, max(5, args.steps // 5)) / reps
+    top_bytes = rows[lvl] * V * 2 + rows[lvl] * 8 + B * k * 12
     achieved = top_bytes / (top_ms * 1e-3) / 1e9
     step_gbs = alg["bytes"] / (ms * 1e-3) / 1e9
-    log(f"step {ms * 1e3:.1f} us ({step_gbs:.0f} GB/s over all levels); top-k of {rows[lvl]} rows "
+    log(f"step {ms * 1e3:.1f} us ({step_gbs:.0f} GB/s over all levels); one level of {rows[lvl]} rows "
         f"{top_ms * 1e3:.2f} us = {achieved:.0f} GB/s")
 
     res = {
@@ -1079,8 +1073,7 @@ def bench_treegrow(args, torch, K, W):
                    "step_effective_gbs": round(step_gbs, 1)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
-                     "kernel": f"topk_chunk_kernel + topk_merge_kernel on one level of {rows[lvl]} rows "
-                               f"(timed together)",
+                     "kernel": f"topk_chunk_kernel<bf16, level> on one level of {rows[lvl]} rows",
                      "algorithmic_bytes_per_launch": top_bytes},
     }
     if not args.no_cpu_baseline:

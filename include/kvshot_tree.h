@@ -12,6 +12,7 @@
  *   2. kvshot_tree_expand: per sequence, the k best children of the frontier,
  *      a child (f, v) scoring score(f) + logprob (ties: smaller frontier index,
  *      then better proposal rank);
+ *   (kvshot_tree_level does 1 and 2 for one level in a single launch.)
  *   3. kvshot_tree_select: per sequence, the n best frontier nodes of all levels
  *      (ties: shallower, then earlier in its level) as a tree ordered by depth,
  *      then rank, with parents indexing that order (-1: a child of the root).
@@ -64,6 +65,33 @@ kvshot_status kvshot_topk_logprobs(const void* logits, int32_t dtype, int32_t ro
 kvshot_status kvshot_tree_expand(int32_t batch, int32_t frontier, int32_t proposals, int32_t k, const float* scores,
                                  const int32_t* tokens, const float* logprobs, int32_t* next_parent,
                                  int32_t* next_tokens, float* next_scores, void* stream);
+
+/* Bytes of workspace kvshot_tree_level needs: 17 * 256 bytes of counters per
+ * sequence, then 136 bytes per frontier row and per (frontier row, chunk of
+ * 16384 logits).  -1 for batch < 1, frontier outside 1..16, vocab < 1 or
+ * vocab > 64 * 16384. */
+int64_t kvshot_tree_level_workspace_bytes(int32_t batch, int32_t frontier, int32_t vocab);
+
+/* One level of growth in one launch: the same result as kvshot_topk_logprobs
+ * over the batch * frontier rows followed by kvshot_tree_expand with
+ * proposals = k (bit for bit: the same float32 operations in the same order).
+ * logits    row b * frontier + f (frontier node f of sequence b) at
+ *           logits + (b * frontier + f) * row_stride, `vocab` values each;
+ *           dtype, alignment and row_stride as for kvshot_topk_logprobs
+ * scores    float32 [batch][frontier]: the frontier's scores (zeros for the root)
+ * next_parent, next_tokens int32 [batch][k], next_scores float32 [batch][k]
+ * workspace device scratch of workspace_bytes >= kvshot_tree_level_workspace_bytes,
+ *           256-byte aligned.  Its counters must be zero before the first call
+ *           (fill the workspace with zeros once); every call leaves them zero.
+ *           Calls with any frontier size may share a workspace sized for the
+ *           largest; a call with another batch size needs a workspace of its
+ *           own (or one filled with zeros again).  Calls that share a
+ *           workspace must not run concurrently.
+ * 1 <= frontier <= 16, 1 <= k <= 16, k <= vocab <= 64 * 16384. */
+kvshot_status kvshot_tree_level(const void* logits, int32_t dtype, int32_t batch, int32_t frontier, int32_t vocab,
+                                int64_t row_stride, int32_t k, const float* scores, int32_t* next_parent,
+                                int32_t* next_tokens, float* next_scores, void* workspace, int64_t workspace_bytes,
+                                void* stream);
 
 /* level_parent, level_tokens int32 [depth][batch][k], level_scores float32 [depth][batch][k]:
  *           kvshot_tree_expand's outputs of levels 1 .. depth, each level one contiguous

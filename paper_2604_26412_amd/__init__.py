@@ -35,6 +35,7 @@ EXPORTED_SYMBOLS = [
     "kvshot_kvproj_init", "kvshot_kvproj_destroy", "kvshot_kv_project", "kvshot_kv_project_validate",
     "kvshot_kvproj_set_option", "kvshot_kvproj_plan", "kvshot_kvproj_profile_read",
     "kvshot_acceptance_stats", "kvshot_topk_workspace_bytes", "kvshot_topk_logprobs", "kvshot_tree_expand", "kvshot_tree_select",
+    "kvshot_tree_level_workspace_bytes", "kvshot_tree_level",
 ]
 FUSION_CROSS_ONLY, FUSION_OUT_FP32 = 1, 2
 KVPROJ_ROPE = 1
@@ -135,6 +136,7 @@ def load_library(path: Optional[str] = None):
         "kvshot_topk_logprobs": [_vp, _i32, _i32, _i32, _i64, _i32, _vp, _vp, _vp, _i64, _vp],
         "kvshot_tree_expand": [_i32, _i32, _i32, _i32] + [_vp] * 6 + [_vp],
         "kvshot_tree_select": [_i32, _i32, _i32, _i32] + [_vp] * 7 + [_vp],
+        "kvshot_tree_level": [_vp, _i32, _i32, _i32, _i32, _i64, _i32] + [_vp] * 5 + [_i64, _vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -142,6 +144,8 @@ def load_library(path: Optional[str] = None):
         f.restype = ctypes.c_int
     lib.kvshot_topk_workspace_bytes.argtypes = [_i32, _i32]
     lib.kvshot_topk_workspace_bytes.restype = _i64
+    lib.kvshot_tree_level_workspace_bytes.argtypes = [_i32, _i32, _i32]
+    lib.kvshot_tree_level_workspace_bytes.restype = _i64
     lib.kvshot_status_string.argtypes = [_i32]
     lib.kvshot_status_string.restype = ctypes.c_char_p
     if path is None:
@@ -493,6 +497,41 @@ def tree_select(level_parent, level_tokens, level_scores, n: int, stream=None):
     return out[0], out[1], out[2], osc
 
 
+def tree_level_workspace(batch: int, frontier: int, vocab: int, device="cuda"):
+    """A zero-filled workspace for ``tree_level`` (its counters must start at zero; calls leave them so)."""
+    torch = _torch()
+    n = load_library().kvshot_tree_level_workspace_bytes(int(batch), int(frontier), int(vocab))
+    if n < 0:
+        raise ValueError(f"no tree-level plan for batch={batch}, frontier={frontier}, vocab={vocab}")
+    return torch.zeros(int(n), dtype=torch.uint8, device=device)
+
+
+def tree_level(logits, scores, k: int, workspace=None, out=None, stream=None):
+    """One level of growth in one launch: ``logits`` [batch][F][vocab] (bf16 or float32, rows contiguous),
+    ``scores`` [batch][F] float32 -> next frontier (parent index, token, score; each [batch][k])."""
+    torch = _torch()
+    lib = load_library()
+    if logits.dtype not in (torch.bfloat16, torch.float32) or not logits.is_cuda or logits.dim() != 3 \
+            or not logits.is_contiguous():
+        raise ValueError("logits must be a contiguous bf16 or float32 device tensor [batch][frontier][vocab]")
+    batch, frontier, vocab = logits.shape
+    sc = GatedDeltaFusion._tensor(scores, "scores", torch.float32, (batch, frontier))
+    if workspace is None:
+        workspace = tree_level_workspace(batch, frontier, vocab, logits.device)
+    if out is None:
+        out = (torch.empty((batch, k), dtype=torch.int32, device=logits.device),
+               torch.empty((batch, k), dtype=torch.int32, device=logits.device),
+               torch.empty((batch, k), dtype=torch.float32, device=logits.device))
+    par, tok, nsc = out
+    for t, name, dt in ((par, "parent", torch.int32), (tok, "token", torch.int32), (nsc, "score", torch.float32)):
+        GatedDeltaFusion._tensor(t, name, dt, (batch, k))
+    _check("kvshot_tree_level", lib.kvshot_tree_level(
+        logits.data_ptr(), BF16 if logits.dtype == torch.bfloat16 else FP32, batch, frontier, vocab, vocab, k, sc,
+        par.data_ptr(), tok.data_ptr(), nsc.data_ptr(), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream_of(stream)))
+    return par, tok, nsc
+
+
 def grow_tree(level_logits, k: int, n: int, stream=None):
     """Grow a tree level by level: ``level_logits[d]`` holds the drafter's logits for level d's frontier
     ([batch][1][vocab] for the root, then [batch][k][vocab], frontier nodes in the order the previous level
@@ -506,11 +545,9 @@ def grow_tree(level_logits, k: int, n: int, stream=None):
     lsc = torch.empty((depth, batch, k), dtype=torch.float32, device=dev)
     scores = torch.zeros((batch, 1), dtype=torch.float32, device=dev)
     vocab = level_logits[0].shape[-1]
-    need = max(topk_workspace_bytes(z.numel() // vocab, vocab) for z in level_logits)
-    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ws = tree_level_workspace(batch, max(z.shape[1] for z in level_logits), vocab, dev)
     for d, z in enumerate(level_logits):
-        tok, lp = topk_logprobs(z, k, workspace=ws, stream=stream)
-        tree_expand(scores, tok, lp, k, out=(lpar[d], ltok[d], lsc[d]), stream=stream)
+        tree_level(z, scores, k, workspace=ws, out=(lpar[d], ltok[d], lsc[d]), stream=stream)
         scores = lsc[d]
     return tree_select(lpar, ltok, lsc, n, stream)
 

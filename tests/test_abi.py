@@ -252,3 +252,20 @@ def test_tree_calls_reject_bad_arguments_before_any_device_call(lib):
     assert sel(2, 8, 10, 81, ok, ok, ok, ok, ok, ok, ok, None) == 1       # n > depth * k
     assert sel(2, 8, 10, 0, ok, ok, ok, ok, ok, ok, ok, None) == 1
     assert sel(2, 8, 10, 60, ok, ok, ok, ok, ok, None, ok, None) == 1
+
+
+def test_tree_level_workspace_sizes_and_rejections(lib):
+    f = lib.kvshot_tree_level_workspace_bytes
+    assert f(8, 10, 151936) == 8 * 17 * 256 + 8 * 10 * 11 * 136
+    assert f(65, 1, 100) == 65 * 17 * 256 + 65 * 2 * 136
+    assert f(0, 10, 100) == -1 and f(8, 17, 100) == -1 and f(8, 10, 64 * 16384 + 1) == -1
+    ok = ctypes.c_void_p(256)
+    lv = lib.kvshot_tree_level
+    need = f(2, 10, 100)
+    assert lv(ok, 0, 2, 17, 100, 104, 10, ok, ok, ok, ok, ok, need, None) == 1          # frontier > 16
+    assert lv(ok, 0, 2, 10, 100, 104, 17, ok, ok, ok, ok, ok, need, None) == 1          # k > 16
+    assert lv(ok, 0, 2, 10, 5, 8, 10, ok, ok, ok, ok, ok, need, None) == 1              # k > vocab
+    assert lv(ok, 0, 2, 10, 100, 104, 10, ok, ok, ok, ok, ok, need - 1, None) == 1      # workspace too small
+    assert lv(ok, 0, 2, 10, 100, 104, 10, ok, ok, ok, ok, ctypes.c_void_p(264), need, None) == 1   # not 256-aligned
+    assert lv(ok, 0, 2, 10, 100, 104, 10, None, ok, ok, ok, ok, need, None) == 1        # scores missing
+    assert lv(ok, 0, 0, 10, 100, 104, 10, ok, ok, ok, ok, ok, need, None) == 1

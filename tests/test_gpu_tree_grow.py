@@ -219,6 +219,96 @@ def test_two_token_vocabulary_example():
     assert depths.cpu().numpy().tolist() == [[0, 0, 1, 2]]
 
 
+# ---------------------------------------------------------------- one level in one launch
+
+
+def topk_then_expand(logits, scores, k):
+    tok, lp = K().topk_logprobs(logits, k)
+    return K().tree_expand(scores, tok, lp, k)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("B,F,V,k", [(8, 10, 151936, 10), (8, 1, 151936, 10), (3, 16, 40000, 16), (5, 7, 16384, 3),
+                                     (2, 4, 5000, 1), (4, 2, 1000003, 16), (1, 3, 20, 16)])
+def test_tree_level_equals_topk_then_expand(dtype, B, F, V, k):
+    # the fused level and the two separate calls make the same float32 operations in the same order
+    t = G.torch()
+    host = W.draft_logits(7600 + V % 97 + F, B * F, V, dtype=dtype, stream=k).reshape(B, F, V)
+    dev = to_dev(host, dtype)
+    rng = np.random.default_rng(V + F)
+    scores = t.from_numpy(-rng.uniform(0, 8, size=(B, F)).astype(np.float32)).cuda()
+    got = K().tree_level(dev, scores, k)
+    want = topk_then_expand(dev, scores, k)
+    t.cuda.synchronize()
+    for g, w in zip(got, want):
+        assert np.array_equal(g.cpu().numpy(), w.cpu().numpy())
+
+
+def test_tree_level_workspace_shared_by_frontier_sizes():
+    # the root level (one frontier node) and full levels alternate on one workspace
+    t = G.torch()
+    B, V, k = 3, 40000, 10
+    ws = K().tree_level_workspace(B, k, V)
+    for i, F in enumerate([1, 10, 1, 10, 10, 1]):
+        z = to_dev(W.draft_logits(7900 + i, B * F, V).reshape(B, F, V), "bf16")
+        scores = t.full((B, F), -0.5 * i, device="cuda")
+        got = K().tree_level(z, scores, k, workspace=ws)
+        want = topk_then_expand(z, scores, k)
+        t.cuda.synchronize()
+        for g, w in zip(got, want):
+            assert np.array_equal(g.cpu().numpy(), w.cpu().numpy()), (i, F)
+
+
+def test_tree_level_ties_take_the_arg_max_rounds():
+    # flat rows: more than 1024 logits of a chunk at the threshold
+    t = G.torch()
+    host = W.draft_logits(7700, 2 * 3, 40000, sigma=0.3, peaks=0, grid=1.0).reshape(2, 3, 40000)
+    dev = to_dev(host, "bf16")
+    scores = t.zeros((2, 3), device="cuda")
+    scores[:, 1] = -1.0
+    got = K().tree_level(dev, scores, 16)
+    want = topk_then_expand(dev, scores, 16)
+    t.cuda.synchronize()
+    for g, w in zip(got, want):
+        assert np.array_equal(g.cpu().numpy(), w.cpu().numpy())
+
+
+def test_tree_level_workspace_is_left_clean_for_the_next_call_and_graph_replays():
+    t = G.torch()
+    B, F, V, k = 4, 10, 60000, 10
+    ws = K().tree_level_workspace(B, F, V)
+    levels = [to_dev(W.draft_logits(7800, B * F, V, stream=i).reshape(B, F, V), "bf16") for i in range(3)]
+    scores = t.zeros((B, F), device="cuda")
+    outs = [K().tree_level(z, scores, k, workspace=ws) for z in levels]
+    t.cuda.synchronize()
+    for z, o in zip(levels, outs):
+        w = topk_then_expand(z, scores, k)
+        for g, r in zip(o, w):
+            assert np.array_equal(g.cpu().numpy(), r.cpu().numpy())
+    assert int(ws[:256 * B * 17].view(t.int32).abs().sum()) == 0     # the counters are back at zero
+    # captured once, replayed three times with eager work between the replays
+    src = levels[0].clone()
+    out = tuple(t.empty((B, k), dtype=dt, device="cuda") for dt in (t.int32, t.int32, t.float32))
+    graph = t.cuda.CUDAGraph()
+    side = t.cuda.Stream()
+    side.wait_stream(t.cuda.current_stream())
+    with t.cuda.stream(side):
+        K().tree_level(src, scores, k, workspace=ws, out=out)
+    t.cuda.current_stream().wait_stream(side)
+    t.cuda.synchronize()
+    with t.cuda.graph(graph):
+        K().tree_level(src, scores, k, workspace=ws, out=out)
+    for z in levels:
+        src.copy_(z)
+        t.cuda.synchronize()
+        graph.replay()
+        t.cuda.synchronize()
+        w = topk_then_expand(z, scores, k)
+        t.cuda.synchronize()
+        for g, r in zip(out, w):
+            assert np.array_equal(g.cpu().numpy(), r.cpu().numpy())
+
+
 # ---------------------------------------------------------------- whole growth from logits
 
 
@@ -316,6 +406,14 @@ def test_binding_rejects_bad_arguments():
     big = t.zeros((4, 20000), dtype=t.bfloat16, device="cuda")
     with pytest.raises(K().KvshotError):
         K().topk_logprobs(big, 4, workspace=t.empty(16, dtype=t.uint8, device="cuda"))
+    with pytest.raises((ValueError, K().KvshotError)):      # no workspace plan for 17 frontier nodes
+        K().tree_level(t.zeros((2, 17, 100), dtype=t.bfloat16, device="cuda"), t.zeros((2, 17), device="cuda"), 4)
+    with pytest.raises(K().KvshotError):
+        K().tree_level(t.zeros((2, 17, 100), dtype=t.bfloat16, device="cuda"), t.zeros((2, 17), device="cuda"), 4,
+                       workspace=t.zeros(1 << 16, dtype=t.uint8, device="cuda"))
+    with pytest.raises(K().KvshotError):
+        K().tree_level(t.zeros((2, 3, 20000), dtype=t.bfloat16, device="cuda"), t.zeros((2, 3), device="cuda"), 4,
+                       workspace=t.zeros(256, dtype=t.uint8, device="cuda"))
     sc = t.zeros((2, 17), device="cuda")
     with pytest.raises(K().KvshotError):
         K().tree_expand(sc, t.zeros((2, 17, 4), dtype=t.int32, device="cuda"),
