@@ -12,11 +12,13 @@
 //   * a threshold T: the k-th largest of the maxima of the 16 lane rows (16
 //     lanes x 64 logits each).  Those k maxima are k distinct logits >= T, so
 //     every logit of the chunk's top k is >= T;
-//   * the logits >= T (threads whose max is below T skip the scan) are
-//     appended to an LDS list, usually a few dozen, and ranked by counting
-//     the entries that beat each one.  Should more than 1024 pass (a flat
-//     distribution with many equal logits), k rounds of workgroup arg-max
-//     over the registers give the same k pairs.
+//   * the logits >= T are appended to an LDS list, usually a few dozen, and
+//     ranked by counting the entries that beat each one.  Threads first
+//     append their groups of 8 logits whose max is >= T, and one thread per
+//     group then appends that group's logits >= T.  Should more than 256
+//     groups or 1024 logits pass (a flat distribution with many equal
+//     logits), k rounds of workgroup arg-max over the registers give the same
+//     k pairs.
 // Reductions across lanes use DPP moves within 16-lane rows and lane reads
 // across rows; no LDS round trip.  A pair (logit, token) travels as one
 // 64-bit key -- the logit's bits mapped to an unsigned order, then the
@@ -55,6 +57,7 @@ constexpr int kPerThread = 64;                  // logits per thread, in registe
 constexpr int kChunk = kThreads * kPerThread;   // logits per workgroup
 constexpr int kMaxChunks = 64;                  // vocabulary <= 64 chunks
 constexpr int kCandCap = 1024;                  // threshold-passing logits kept in LDS
+constexpr int kSlots = kThreads;                // threshold-passing groups of 8 logits kept in LDS
 constexpr int kRecord = kTopK + 1;              // workspace words (64-bit) per chunk: keys, then (m, s)
 constexpr int kCounterStride = 64;              // 32-bit words between two arrival counters: a 256-byte line
                                                 // each, since device atomics on one line serialize
@@ -200,8 +203,10 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
   __shared__ float row_m[16], row_s[16];
   __shared__ float sh_T, sh_M, sh_S;
   __shared__ uint64_t win[4];
-  __shared__ uint64_t cand[kCandCap];
-  __shared__ int cand_n;
+  __shared__ uint64_t cand[kCandCap + 1];         // + a spare slot for writes that are thrown away
+  __shared__ float4 slot_v[kSlots][2];
+  __shared__ int slot_t[kSlots];
+  __shared__ int cand_n, slot_n;
   __shared__ int sh_last;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row = blockIdx.x / chunks;
@@ -277,9 +282,15 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
   auto off = [](int i) { return 8 * kThreads * (i >> 3) + (i & 7); };
 
   // the thread's log-sum-exp part, then its row's
+  float gm[kPerThread / 8];                       // max of each group of 8: the scan below skips groups
   float mt = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < kPerThread; ++i) mt = fmaxf(mt, z[i]);
+  for (int g = 0; g < kPerThread / 8; ++g) {
+    gm[g] = z[8 * g];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) gm[g] = fmaxf(gm[g], z[8 * g + e]);
+    mt = fmaxf(mt, gm[g]);
+  }
   float st = 0.0f;
   if (mt != -INFINITY) {
     const float off = mt * kLog2e;
@@ -292,7 +303,10 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
     row_m[tid >> 4] = mr;
     row_s[tid >> 4] = sr;
   }
-  if (tid == 0) cand_n = 0;
+  if (tid == 0) {
+    cand_n = 0;
+    slot_n = 0;
+  }
   __syncthreads();
   if (tid < 16) {
     // lanes 0..15 of wave 0 -- one DPP row -- hold the 16 lane rows' parts: the chunk's (M, S), and
@@ -315,24 +329,46 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
   __syncthreads();
   const float T = fmaxf(sh_T, -FLT_MAX);           // never below the smallest logit: -inf never passes
 
-  // logits >= T into the LDS list: count, one LDS atomic per thread, then write
-  int cnt = 0;
+  // logits >= T into the LDS list, in two steps that spread the work over the threads: every
+  // thread appends its groups of 8 whose max is >= T (the 8 logits and the first token) to a slot
+  // list; then thread t turns slot t into the keys of its logits >= T.
+  int gcnt = 0;
   if (mt >= T) {
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i) cnt += z[i] >= T ? 1 : 0;
+    for (int g = 0; g < kPerThread / 8; ++g) gcnt += gm[g] >= T ? 1 : 0;
   }
-  if (cnt > 0) {
-    int p = atomicAdd(&cand_n, cnt);
+  if (gcnt > 0) {
+    int p = atomicAdd(&slot_n, gcnt);
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i) {
-      if (z[i] >= T) {
-        if (p < kCandCap) cand[p] = pair_key(z[i], tbase + off(i));
+    for (int g = 0; g < kPerThread / 8; ++g)
+      if (gm[g] >= T) {
+        if (p < kSlots) {
+          slot_v[p][0] = float4{z[8 * g], z[8 * g + 1], z[8 * g + 2], z[8 * g + 3]};
+          slot_v[p][1] = float4{z[8 * g + 4], z[8 * g + 5], z[8 * g + 6], z[8 * g + 7]};
+          slot_t[p] = tbase + off(8 * g);
+        }
         ++p;
       }
+  }
+  __syncthreads();
+  const int ns = slot_n;
+  if (ns <= kSlots && tid < ns) {
+    const float4 a = slot_v[tid][0], c = slot_v[tid][1];
+    const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cnt += v[e] >= T ? 1 : 0;
+    int p = atomicAdd(&cand_n, cnt);
+    const int t0 = slot_t[tid];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {                 // branch-free: a logit below T goes to the spare slot
+      const bool pass = v[e] >= T;
+      cand[pass && p < kCandCap ? p : kCandCap] = pair_key(v[e], t0 + e);
+      p += pass ? 1 : 0;
     }
   }
   __syncthreads();
-  const int n = cand_n;
+  const int n = ns <= kSlots ? cand_n : kCandCap + 1;   // too many groups: the arg-max rounds below
 
   const bool final_row = !LEVEL && chunks == 1;
   const float lse = sh_M + logf(sh_S);
@@ -404,6 +440,8 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
 
   __shared__ uint64_t parts[kMaxChunks];          // (m, s) of the row's chunk j
   __shared__ uint64_t ekeys[kMaxCand];
+  // Each chunk's keys are sorted, best first, so the largest of the chunks' k-th keys is below or
+  // at the row's k-th key: only keys at or above it can be among the row's k best.
   const uint64_t* rrec = ws + (int64_t)row * chunks * kRecord;
   const int per_row = chunks * k;                 // <= 1024 keys
   for (int c = tid; c < per_row; c += kThreads) {
@@ -411,11 +449,31 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
     cand[c] = load_rec(rrec + j * kRecord + (c - j * k));
   }
   if (tid < chunks) parts[tid] = load_rec(rrec + tid * kRecord + kTopK);
+  if (tid == 0) cand_n = 0;
   __syncthreads();
-  uint64_t* rowrec = L.rows + (int64_t)row * kRecord;
+  if (tid < 64) {                                 // chunks <= 64: one lane per chunk
+    const uint64_t kth = wave_max(tid < chunks ? cand[tid * k + k - 1] : (uint64_t)0);
+    if (tid == 0) win[0] = kth;
+  }
+  __syncthreads();
+  const uint64_t floor_key = win[0];
+  uint64_t* top = cand + per_row;                 // the keys that pass, after the row's keys
+  const int room = kCandCap - per_row;
   for (int c = tid; c < per_row; c += kThreads) {
     const uint64_t key = cand[c];
-    const int rank = rank_of(cand, per_row, key);
+    if (key >= floor_key) {
+      const int p = atomicAdd(&cand_n, 1);
+      if (p < room) top[p] = key;
+    }
+  }
+  __syncthreads();
+  const int m = cand_n;
+  const uint64_t* pool = m <= room ? top : cand;  // no room left after the row's keys: rank them all
+  const int pn = m <= room ? m : per_row;
+  uint64_t* rowrec = L.rows + (int64_t)row * kRecord;
+  for (int c = tid; c < pn; c += kThreads) {
+    const uint64_t key = pool[c];
+    const int rank = rank_of(pool, pn, key);
     if (rank < k) store_rec(rowrec + rank, key);
   }
   if (tid == 0) {
