@@ -963,6 +963,27 @@ def bench_accept(args, torch, K, W):
 TREEGROW_METRIC = "level-wise draft-tree growth (depth 8, top-k 10, 60 nodes) from bf16 logits: trees/s"
 
 
+def treegrow_source_hash() -> str:
+    h = hashlib.sha256()
+    h.update(open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", "tree_grow.hip"), "rb").read())
+    h.update(open(os.path.join(ROOT, "include", "kvshot_tree.h"), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_treegrow_traffic(workload: str):
+    """HBM bytes of one 80-row level launch from a committed counter summary, if it matches this source."""
+    path = os.path.join(PROFILES, f"topk_chunk_kernel_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not (m and f and w) or m.group(1) != treegrow_source_hash():
+        return None
+    return float(f.group(1)) + float(w.group(1))
+
+
 def capture(torch, fn):
     """A HIP graph of fn() (one eager run on a side stream first, as torch asks)."""
     graph = torch.cuda.CUDAGraph()
@@ -1072,7 +1093,7 @@ def bench_treegrow(args, torch, K, W):
                    "launch": "python" if args.no_graph else "hip graph replay",
                    "step_effective_gbs": round(step_gbs, 1)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": read_treegrow_traffic(name),
                      "kernel": f"topk_chunk_kernel<bf16, level> on one level of {rows[lvl]} rows",
                      "algorithmic_bytes_per_launch": top_bytes},
     }
