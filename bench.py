@@ -240,6 +240,8 @@ def main():
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--path", choices=["auto", "mfma", "generic"], default="auto",
+                    help="attention kernel: the planner's choice (bf16: MFMA), or forced")
     ap.add_argument("--cold", action="store_true",
                     help="flush the device caches (write 1 GiB) before every timed call; per-call events")
     ap.add_argument("--no-graph", action="store_true",
@@ -290,6 +292,8 @@ def main():
                            rope_theta=d["theta"], softmax_scale=d["scale"])
     if args.splits:
         att.set_option(K.OPT_SPLITS, args.splits)
+    if args.path != "auto":
+        att.set_option(K.OPT_PATH, {"mfma": 1, "generic": 2}[args.path])
     nq_call = n if args.mode == "folded" else 1
     plan = att.plan(B, nq_call, T_max)
     edt = torch.bfloat16 if d["dtype"] == "bf16" else torch.float32
@@ -384,7 +388,7 @@ def main():
 
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     achieved = attn_launch_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = read_traffic(args.workload, args.mode) if not args.splits else None
+    traffic = read_traffic(args.workload, args.mode) if not args.splits and plan["path"] == 1 else None
     path_name = {1: "attn_mfma_kernel", 2: "attn_generic_kernel"}[plan["path"]]
     kernel = f"{path_name} ({plan['row_tiles']} x 32-row query tiles per (sequence, KV head))" \
         if plan["path"] == 1 else path_name
@@ -409,7 +413,8 @@ def main():
                                f"{d['dtype']}, {P}-token pages, random page table",
                    "batch": B, "ctx_len_max": T_max, "draft_queries": n, "mode": args.mode if d["mode"] == "step"
                    else "tree", "page_size": P, "splits": plan["splits"], "workgroups": plan["workgroups"],
-                   "cold_caches": bool(args.cold), "launch": "python" if args.no_graph else "hip graph replay"},
+                   "cold_caches": bool(args.cold), "launch": "python" if args.no_graph else "hip graph replay",
+                   "path": {1: "mfma", 2: "generic"}[plan["path"]]},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel,
                      "kernel_ms": round(attn_ms, 5), "combine_ms": round(comb_ms, 5),
