@@ -60,8 +60,9 @@ def read_traffic(workload: str, mode: str):
 # workloads on the device
 # ---------------------------------------------------------------------------
 
-def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=128, P=16):
-    """Seeded device-side generator for the 64 x 32768 workload (values N(0,1), bf16, random page table)."""
+def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=128, P=16, contiguous=False):
+    """Seeded device-side generator for the 64 x 32768 workload (values N(0,1), bf16, random page table;
+    ``contiguous``: sequence b owns pages b * T / P onward, in order)."""
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     pps = T // P
@@ -71,6 +72,8 @@ def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=1
     kp = torch.randn((pool, Hkv, P, D), generator=g, device=dev, dtype=torch.bfloat16)
     vp = torch.randn((pool, Hkv, P, D), generator=g, device=dev, dtype=torch.bfloat16)
     perm = torch.randperm(pool, generator=g, device=dev)
+    if contiguous:
+        perm = torch.arange(pool, device=dev)
     table = perm[:used].view(B, pps).to(torch.int32).contiguous()
     spare = perm[used:]
     kp[spare] = float("nan")
@@ -240,6 +243,11 @@ def main():
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--contiguous", action="store_true",
+                    help="64 x 32K workload: contiguous page table instead of a random permutation")
+    ap.add_argument("--calls", type=int, default=None,
+                    help="per-call timing sample for the median and p10/p90 (default: 100 for the 64 x 32K "
+                         "workload, 200 otherwise; 0 skips it)")
     ap.add_argument("--path", choices=["auto", "mfma", "generic"], default="auto",
                     help="attention kernel: the planner's choice (bf16: MFMA), or forced")
     ap.add_argument("--cold", action="store_true",
@@ -278,7 +286,9 @@ def main():
         raise SystemExit("fusion workloads run with --op fusion")
     if args.workload == DEFAULT_WORKLOAD:
         log("generating the 64 x 32768 workload on the device")
-        d = make_long_range_on_device(torch, args.seed)
+        d = make_long_range_on_device(torch, args.seed, contiguous=args.contiguous)
+    elif args.contiguous:
+        raise SystemExit("--contiguous applies to the 64 x 32K workload only")
     else:
         log(f"generating {args.workload} on the host")
         d = upload_case(torch, W.workload(args.workload))
@@ -373,6 +383,23 @@ def main():
         torch.cuda.synchronize()
         ms_per_step = e0.elapsed_time(e1) / args.steps
 
+    # per-call distribution: each replay between its own pair of events (median, p10, p90)
+    ncalls = args.calls if args.calls is not None else (100 if args.workload == DEFAULT_WORKLOAD else 200)
+    call_ms = None
+    if ncalls > 0 and not args.cold:
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(ncalls)]
+        torch.cuda.synchronize()
+        for a, z in evs:
+            a.record(stream)
+            run_step()
+            z.record(stream)
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(z) for a, z in evs)
+        call_ms = {"calls": ncalls, "median": round(ts[ncalls // 2], 5), "p10": round(ts[ncalls // 10], 5),
+                   "p90": round(ts[(9 * ncalls) // 10], 5)}
+        log(f"per call over {ncalls}: median {call_ms['median']:.4f} ms, p10 {call_ms['p10']:.4f}, "
+            f"p90 {call_ms['p90']:.4f}")
+
     # per-kernel durations from HIP events the library records around each launch on this stream
     att.set_option(K.OPT_PROFILE, 1)
     for _ in range(args.steps):
@@ -414,7 +441,9 @@ def main():
                    "batch": B, "ctx_len_max": T_max, "draft_queries": n, "mode": args.mode if d["mode"] == "step"
                    else "tree", "page_size": P, "splits": plan["splits"], "workgroups": plan["workgroups"],
                    "cold_caches": bool(args.cold), "launch": "python" if args.no_graph else "hip graph replay",
-                   "path": {1: "mfma", 2: "generic"}[plan["path"]]},
+                   "path": {1: "mfma", 2: "generic"}[plan["path"]],
+                   "page_table": "contiguous" if args.contiguous else "random permutation"},
+        "call_ms": call_ms,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel,
                      "kernel_ms": round(attn_ms, 5), "combine_ms": round(comb_ms, 5),
