@@ -67,8 +67,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ---- keys: larger key = larger value, then smaller index
 
+// -0 + 0 = +0, so both zeros get one key: equal values tie, as in every float comparison
 __device__ __forceinline__ uint32_t ordered(float v) {
-  const uint32_t b = __float_as_uint(v);
+  const uint32_t b = __float_as_uint(v + 0.0f);
   return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
 }
 

@@ -95,6 +95,19 @@ def test_topk_all_equal_row_and_single_winner():
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("vocab", [300, 40000])
+def test_topk_treats_both_zeros_as_equal(dtype, vocab):
+    # the 16th best logit falls among zeros of both signs: -0.0 and +0.0 tie, the smaller token wins
+    z = np.full((2, vocab), -3.0, np.float32)
+    z[:, :6] = 2.0
+    zeros = np.arange(50, vocab, max(1, vocab // 40))[:30]
+    z[0, zeros] = np.where(np.arange(len(zeros)) % 2 == 0, np.float32(-0.0), np.float32(0.0))
+    z[1, zeros] = np.where(np.arange(len(zeros)) % 2 == 0, np.float32(0.0), np.float32(-0.0))
+    host = W.f32_to_bf16_bits(z) if dtype == "bf16" else z
+    check_topk(host, dtype, 16)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_topk_honours_the_row_stride(dtype):
     # rows of 151936 logits inside rows of 152000: the padding holds larger values that must be ignored
     vocab, stride = 151936, 152000
