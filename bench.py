@@ -471,7 +471,7 @@ FUSION_METRIC = "gated-delta fusion tokens/s (d=4096, bf16) with achieved TFLOP/
 
 def fusion_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("fusion.hip", "fusion_common.h", "kvshot_common.h"):
+    for f in ("fusion.hip", "fusion_common.h", "kvshot_common.h", "fusion_api.cpp"):
         h.update(open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 

@@ -39,16 +39,18 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 int m_tiles_of(int tokens) { return (tokens + kFusionTokens - 1) / kFusionTokens; }
 
 // Reduction splits: the largest power of two (<= 8) that keeps the grid within
-// one workgroup per CU, then capped by the workspace.  (16 splits at two
-// workgroups per CU measured slower: the larger partial sum costs more in the
-// combine than the main kernel gains.)
+// two workgroups per CU (two resident workgroups hide each other's per-chunk
+// latency: d = 4096, graph replay, 128 tokens 62 -> 50 us with 8 splits instead
+// of 4, 480 tokens 121 -> 107 us with 2 instead of 1, other sizes unchanged),
+// then capped by the workspace.  (16 splits measured slower: the larger partial
+// sum costs more in the combine than the main kernel gains.)
 int plan_splits(const kvshot_fusion_ctx* c, int tokens) {
   const int64_t tiles = (int64_t)m_tiles_of(tokens) * (c->d / kFusionChannels);
   int s = 1;
   if (c->opt_splits > 0) {
     s = c->opt_splits;
   } else {
-    while (s < 8 && tiles * s * 2 <= c->num_cus) s *= 2;
+    while (s < 8 && tiles * s * 2 <= 2 * (int64_t)c->num_cus) s *= 2;
   }
   while (s > 1 && (size_t)s * tokens * c->d > c->ws_pairs) s /= 2;
   return s;
