@@ -21,9 +21,10 @@ level-wise best-first growth:
 
 Pins (tests/test_oracle_tree_grow_pins.py): top-k against a plain scan of tiny
 vocabularies; log-probabilities exponentiate and sum to 1; k = 1 gives the
-greedy chain; a full tree (n = depth k) keeps every frontier node; an
-exhaustive best-first search over every path of tiny trees; ancestor closure
-and topological order on random cases.
+greedy chain; a hand-derived two-token example; a full tree (n = depth k)
+keeps every frontier node; one level against a brute force over every
+(frontier node, vocabulary token) pair; ancestor closure, topological order
+and the n best on random cases.
 """
 from __future__ import annotations
 

@@ -104,3 +104,30 @@ def test_full_tree_keeps_every_frontier_node():
     parents, tokens, depths, scores = grow_tree(levels, 3, 12)
     assert depths.tolist() == [0] * 3 + [1] * 3 + [2] * 3 + [3] * 3
     assert finalize([(np.zeros(2, np.int32), np.array([5, 6], np.int32), np.array([-1.0, -2.0]))], 1)[1].tolist() == [5]
+
+
+def brute_force_level(scores, z, k):
+    """The k best children over every (frontier node, vocabulary token) pair, with the full log-softmax of
+    each row; ties by the smaller frontier index, then the larger logit, then the smaller token id."""
+    F, V = z.shape
+    cand = []
+    for f in range(F):
+        lse = math.log(math.fsum(math.exp(x) for x in z[f]))
+        for v in range(V):
+            cand.append((-(scores[f] + z[f, v] - lse), f, -z[f, v], v))
+    cand.sort()
+    return [(c[1], c[3], -c[0]) for c in cand[:k]]
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_level_equals_brute_force_over_the_whole_vocabulary(seed):
+    # proposing only each node's top k loses no child of the level's k best (and keeps the tie order)
+    rng = np.random.default_rng(100 + seed)
+    F, V, k = 4, 9, 3
+    z = np.round(rng.standard_normal((F, V)) * 2, 0)             # coarse: ties between and within rows
+    scores = np.round(-rng.uniform(0, 3, size=F), 0)
+    tok, lp = log_softmax_topk(z, k)
+    par, t, sc = grow_level(scores, tok, lp, k)
+    want = brute_force_level(scores, z, k)
+    assert [(int(a), int(b)) for a, b in zip(par, t)] == [(f, v) for f, v, _ in want]
+    np.testing.assert_allclose(sc, [s for _, _, s in want], rtol=0, atol=1e-12)
