@@ -52,7 +52,8 @@ Parity status per function:
     final selection of the n best nodes.  The selection rule is a reading
     (the paper gives the shape only): parity unpinned against the paper;
     pinned by a plain scan, a closed-form two-token example, the greedy
-    chain at k = 1 and closure / order / optimality invariants.
+    chain at k = 1, one level against a brute force over the whole
+    vocabulary, and closure / order / optimality invariants.
 """
 from .attention import (  # noqa: F401
     decode,

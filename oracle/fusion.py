@@ -16,7 +16,7 @@ removed from the forward pass; this oracle reads that as n_i = 0 everywhere
 (so Delta_i = o_i), which is a reading, not a printed formula -- parity of the
 cross-only variant is unpinned against the paper.
 
-Pins (tests/test_oracle_pins.py): gate saturated shut reduces to n exactly;
+Pins (tests/test_oracle_fusion_pins.py): gate saturated shut reduces to n exactly;
 gate saturated open with W_Delta = I gives o exactly; the block identity
 W_g [n; o; o - n] = (A - C) n + (B + C) o; a unit Delta selects one column of
 W_Delta; W_g = 0 gives the gate sigmoid(b_g) per channel.
