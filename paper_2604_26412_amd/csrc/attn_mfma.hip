@@ -132,6 +132,17 @@ __device__ __forceinline__ void apply_mask(f32x16& s, uint32_t valid) {
   for (int v = 0; v < 16; ++v) s[v] = ((valid >> v) & 1u) ? s[v] : -INFINITY;
 }
 
+// The value lane l ^ 32 holds, with one VALU lane swap between the wave's halves
+// (v_permlane32_swap: the first result holds the low half in both halves, the
+// second the high half) instead of an LDS permute.  The copy through asm keeps
+// the compiler from treating the two operands as one value.
+__device__ __forceinline__ float other_half(float x) {
+  uint32_t y;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(__float_as_uint(x)));
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), y, false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
 // Branch-free front of the online-softmax update for one block: new reference
 // max, bf16 weights P (as the B operand of O^T += V^T P^T), running sum.
 // Returns through `alpha` the factor the output accumulator must be scaled by
@@ -141,7 +152,7 @@ __device__ __forceinline__ void softmax_front(const f32x16& s, SoftmaxState& st,
   float bm = -INFINITY;
 #pragma unroll
   for (int v = 0; v < 16; ++v) bm = fmaxf(bm, s[v]);
-  bm = fmaxf(bm, __shfl_xor(bm, 32));
+  bm = fmaxf(bm, other_half(bm));
   const bool jump = bm > st.m + kRescaleSlack;   // false while both are -inf
   const float mn = jump ? bm : st.m;
   const float mu = mn == -INFINITY ? 0.0f : mn;
