@@ -144,6 +144,28 @@ __device__ __forceinline__ float rescale(float s, float m, float M) {
   return m == -INFINITY ? 0.0f : s * __builtin_amdgcn_exp2f((m - M) * kLog2e);
 }
 
+// Room for `cnt` (0..8) entries of this lane in an LDS list whose length is
+// `*counter`: the lane's offset among the wave's requests from eight ballots
+// (lane L asks for more than b entries), then one atomic for the whole wave.
+// Called by every lane of the wave (uniform control flow).
+__device__ __forceinline__ int wave_alloc(int cnt, int* counter) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int prefix = 0, total = 0;
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint64_t m = __ballot(cnt > b);
+    prefix += __popcll(m & below);
+    total += __popcll(m);
+  }
+  int base = 0;
+  if (total > 0) {
+    if (lane == 0) base = atomicAdd(counter, total);
+    base = __builtin_amdgcn_readfirstlane(base);
+  }
+  return base + prefix;
+}
+
 // number of the n keys in LDS that beat `key`
 __device__ __forceinline__ int rank_of(const uint64_t* keys, int n, uint64_t key) {
   int rank = 0;
@@ -338,8 +360,9 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
 #pragma unroll
     for (int g = 0; g < kPerThread / 8; ++g) gcnt += gm[g] >= T ? 1 : 0;
   }
+  int p_slot = wave_alloc(gcnt, &slot_n);
   if (gcnt > 0) {
-    int p = atomicAdd(&slot_n, gcnt);
+    int p = p_slot;
 #pragma unroll
     for (int g = 0; g < kPerThread / 8; ++g)
       if (gm[g] >= T) {
@@ -353,19 +376,23 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* logits
   }
   __syncthreads();
   const int ns = slot_n;
-  if (ns <= kSlots && tid < ns) {
-    const float4 a = slot_v[tid][0], c = slot_v[tid][1];
+  if (ns <= kSlots && (tid & ~63) < ns) {         // waves that hold a slot (wave-uniform)
+    const bool mine = tid < ns;
+    const float4 a = mine ? slot_v[tid][0] : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    const float4 c = mine ? slot_v[tid][1] : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
     const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) cnt += v[e] >= T ? 1 : 0;
-    int p = atomicAdd(&cand_n, cnt);
-    const int t0 = slot_t[tid];
+    int p = wave_alloc(cnt, &cand_n);
+    if (mine) {
+      const int t0 = slot_t[tid];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {                 // branch-free: a logit below T goes to the spare slot
-      const bool pass = v[e] >= T;
-      cand[pass && p < kCandCap ? p : kCandCap] = pair_key(v[e], t0 + e);
-      p += pass ? 1 : 0;
+      for (int e = 0; e < 8; ++e) {               // branch-free: a logit below T goes to the spare slot
+        const bool pass = v[e] >= T;
+        cand[pass && p < kCandCap ? p : kCandCap] = pair_key(v[e], t0 + e);
+        p += pass ? 1 : 0;
+      }
     }
   }
   __syncthreads();
