@@ -29,6 +29,10 @@
 // from LDS feeds TPW MFMAs.
 #include "kvshot_common.h"
 
+// 1: a block's V^T operand reads are issued before its softmax
+#ifndef KVSHOT_VREAD_EARLY
+#define KVSHOT_VREAD_EARLY 1
+#endif
 // 1: the eight K operand reads of a block are all issued before its first MFMA
 #ifndef KVSHOT_KREAD_FIRST
 #define KVSHOT_KREAD_FIRST 1
@@ -421,10 +425,47 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
       }
     }
   };
+  // V^T operands of a block: 4 channel tiles x 2 key halves, each two transposed reads
+  auto read_v = [&](const uint16_t* vt, bf16x8 (&vop)[4][2]) {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const __attribute__((address_space(3))) uint16_t* vb =
+        (const __attribute__((address_space(3))) uint16_t*)(vt) + vt_off;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(vb + (16 * sidx) * kVPitch + dt * 32));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(vb + (16 * sidx + 4) * kVPitch + dt * 32));
+        const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+        vop[dt][sidx] = as_bf16x8(u32x4{lo2[0], lo2[1], hi2[0], hi2[1]});
+      }
+    }
+  };
+  auto pv_regs = [&](const u32x4 (&pw)[TPW][2], const bf16x8 (&vop)[4][2]) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx)
+#pragma unroll
+        for (int i = 0; i < TPW; ++i)
+          oacc[i][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][sidx], as_bf16x8(pw[i][sidx]), oacc[i][dt], 0,
+                                                                0, 0);
+  };
   auto softmax_pv_tiles = [&](f32x16 (&sacc)[TPW], const uint16_t* vt, bool masked, const uint32_t (&valid)[TPW]) {
     u32x4 pw[TPW][2];
+#if KVSHOT_VREAD_EARLY
+    // the block's V^T operands are read before the softmax (in the same basic block as the
+    // products before it), so their LDS latency overlaps the softmax instead of following it
+    bf16x8 vop[4][2];
+    read_v(vt, vop);
+    softmax_tiles(sacc, masked, valid, pw);
+    pv_regs(pw, vop);
+#else
     softmax_tiles(sacc, masked, valid, pw);
     pv_tiles(pw, vt);
+#endif
   };
 
   // Stage this wave's share of a block into the LDS tiles; rows at or past
