@@ -1,11 +1,65 @@
 // Cross-split merge of split-K partial softmax states: one wave per query
 // row, the merge itself is combine_row.  (Merging inside the attention kernel,
 // in the last workgroup to finish, measured slower: the device-scope fences it
-// needs write back and invalidate a whole XCD L2 per workgroup.)
+// needs write back and invalidate a whole XCD L2 per workgroup.  The merge has
+// little data to move, so its time is the launch and two dependent loads.)
 #include "kvshot_common.h"
 
 namespace kvshot {
 namespace {
+
+// Merge the split partials of one query row into its output (one wave; every
+// lane takes two channels).  Split s left (m_s, l_s, O_s): its running max
+// (log2 units), its sum of 2^(score - m_s) and its unnormalised output.  The
+// row's result is sum_s O_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s,
+// the softmax-weighted sum over the union of the splits' keys; splits that saw
+// no key (l_s = 0) carry no weight.
+__device__ __forceinline__ void combine_row(const float* part_o, const float2* part_ml, int64_t base, int splits,
+                                            void* out, int64_t orow, bool out_fp32, float* lse_out, int lane) {
+  // Eight splits' rows are loaded at once, with no branch between them, so
+  // their latencies overlap (the first eight also with the (m, l) load); a
+  // split of weight zero is skipped by a select, so whatever its row holds
+  // never reaches the sum.
+  float2 v[8];
+  auto load_rows = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int s = s0 + u < splits ? s0 + u : splits - 1;
+      v[u] = *(const float2*)(part_o + (base + s) * kHeadDim + lane * 2);
+    }
+  };
+  load_rows(0);
+  float ms = -INFINITY, ls = 0.0f;
+  if (lane < splits) {
+    const float2 t = part_ml[base + lane];
+    ms = t.y > 0.0f ? t.x : -INFINITY;
+    ls = t.y;
+  }
+  float M = ms;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  const float Mu = M == -INFINITY ? 0.0f : M;
+  const float wgt = ls > 0.0f ? __builtin_amdgcn_exp2f(ms - Mu) : 0.0f;
+  float L = wgt * ls;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
+  float2 acc = make_float2(0.0f, 0.0f);
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    if (s0 > 0) load_rows(s0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float ws = __shfl(wgt, s0 + u);    // s0 + u < kMaxSplits = 64; lanes past `splits` hold 0
+      acc.x = ws != 0.0f ? acc.x + ws * v[u].x : acc.x;
+      acc.y = ws != 0.0f ? acc.y + ws * v[u].y : acc.y;
+    }
+  }
+  const float inv = 1.0f / L;
+  if (out_fp32)
+    *(float2*)((float*)out + orow + lane * 2) = make_float2(acc.x * inv, acc.y * inv);
+  else
+    *(uint32_t*)((uint16_t*)out + orow + lane * 2) = pack_bf16x2(acc.x * inv, acc.y * inv);
+  if (lse_out && lane == 0) *lse_out = (M + __log2f(L)) * 0.693147180559945309f;
+}
 
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int lane = threadIdx.x & 63;

@@ -95,45 +95,6 @@ __device__ __forceinline__ int64_t kv_offset(int pid, int head, int slot, int64_
   return (int64_t)pid * page_stride + (int64_t)head * head_stride + (int64_t)slot * slot_stride;
 }
 
-// Merge the split partials of one query row into its output (one wave; every
-// lane takes two channels).  Split s left (m_s, l_s, O_s): its running max
-// (log2 units), its sum of 2^(score - m_s) and its unnormalised output.  The
-// row's result is sum_s O_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s,
-// the softmax-weighted sum over the union of the splits' keys; splits that saw
-// no key (l_s = 0) carry no weight.
-__device__ __forceinline__ void combine_row(const float* part_o, const float2* part_ml, int64_t base, int splits,
-                                            void* out, int64_t orow, bool out_fp32, float* lse_out, int lane) {
-  float ms = -INFINITY, ls = 0.0f;
-  if (lane < splits) {
-    const float2 t = part_ml[base + lane];
-    ms = t.y > 0.0f ? t.x : -INFINITY;
-    ls = t.y;
-  }
-  float M = ms;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  const float Mu = M == -INFINITY ? 0.0f : M;
-  const float wgt = ls > 0.0f ? __builtin_amdgcn_exp2f(ms - Mu) : 0.0f;
-  float L = wgt * ls;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
-  float2 acc = make_float2(0.0f, 0.0f);
-  for (int s = 0; s < splits; ++s) {
-    const float ws = __shfl(wgt, s);
-    if (ws != 0.0f) {
-      const float2 v = *(const float2*)(part_o + (base + s) * kHeadDim + lane * 2);
-      acc.x += ws * v.x;
-      acc.y += ws * v.y;
-    }
-  }
-  const float inv = 1.0f / L;
-  if (out_fp32)
-    *(float2*)((float*)out + orow + lane * 2) = make_float2(acc.x * inv, acc.y * inv);
-  else
-    *(uint32_t*)((uint16_t*)out + orow + lane * 2) = pack_bf16x2(acc.x * inv, acc.y * inv);
-  if (lse_out && lane == 0) *lse_out = (M + __log2f(L)) * 0.693147180559945309f;
-}
-
 // The hardware hands workgroup `id` of a 1-D grid to XCD id % 8.  Renumber so
 // that each XCD works through a contiguous range of work items (neighbouring
 // items, which share K/V or page-table rows, then share that XCD's L2).
