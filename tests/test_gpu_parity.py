@@ -166,7 +166,7 @@ def test_draft_lengths(n_new):
     _check_case(c, what=f"n_new {n_new}")
 
 
-@pytest.mark.parametrize("splits", [1, 2, 7, 64])
+@pytest.mark.parametrize("splits", [1, 2, 7, 13, 64])
 def test_split_invariance(splits):
     c = small(ctx_lens=[3000, 2100, 999], n_new=8, seed=71)
     _check_case(c, splits=splits, what=f"splits {splits}")
