@@ -140,6 +140,47 @@ def test_fusion_is_deterministic_and_split_invariant():
     assert np.max(np.abs(outs[1] - outs[8])) <= 1e-4 * (1 + np.max(np.abs(outs[1])))
 
 
+@pytest.mark.parametrize("splits", [1, 8])
+def test_fusion_hip_graph_replay_matches_eager(splits):
+    """A captured call replays to the eager result, with eager work and syncs between replays
+    (split path: the combine kernel is captured too)."""
+    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS
+    t = G.torch()
+    c = W.fusion_case(64, 512, seed=19)
+    with GatedDeltaFusion(512, 64) as fz:
+        fz.set_option(OPT_SPLITS, splits)
+        dv = upload(c)
+        out = t.empty((c.tokens, c.d), dtype=t.bfloat16, device="cuda")
+        gate = t.empty((c.tokens, c.d), dtype=t.float32, device="cuda")
+
+        def call():
+            fz(dv["n"], dv["o"], dv["w_g"], dv["b_g"], dv["w_delta"], out=out, gate=gate)
+        call()
+        t.cuda.synchronize()
+        eager, eager_gate = out.clone(), gate.clone()
+        side = t.cuda.Stream()
+        side.wait_stream(t.cuda.current_stream())
+        with t.cuda.stream(side):
+            call()
+        t.cuda.current_stream().wait_stream(side)
+        t.cuda.synchronize()
+        g = t.cuda.CUDAGraph()
+        with t.cuda.graph(g):
+            call()
+        for rep in range(4):
+            out.zero_()
+            gate.zero_()
+            t.cuda.synchronize()
+            g.replay()
+            t.cuda.synchronize()
+            assert t.equal(out, eager), rep
+            assert t.equal(gate, eager_gate), rep
+            call()                                  # eager work between replays
+            t.cuda.synchronize()
+    ref, _ = reference(c)
+    check(eager.float().cpu().numpy(), ref, False, f"graph splits={splits}")
+
+
 def packed_layout(c):
     """Expected packed copy, by index mapping only: piece (tile, seg, chunk, wave, s, lane) holds
     weights [channel tile*128 + wave*32 + lane%32][chunk*64 + 32*(lane/32) + 8s .. +7] of segment seg."""
