@@ -77,6 +77,37 @@ def test_repeated_calls_restart_from_zero():
         assert c.tolist() == [1000] * 4 + [0] * 4 and m == 4.0
 
 
+def test_hip_graph_replay_matches_eager():
+    """A captured call replays to the eager result (its counts start from zero on every
+    replay), with eager work and syncs between replays."""
+    import paper_2604_26412_amd as Kmod
+    t = G.torch()
+    acc = np.random.default_rng(17).integers(0, 8, size=50_000).astype(np.int32)
+    dev = t.from_numpy(acc).cuda()
+    eager = [x.clone() for x in Kmod.acceptance_stats(dev, 7, retention_step=3)]
+    t.cuda.synchronize()
+    side = t.cuda.Stream()
+    side.wait_stream(t.cuda.current_stream())
+    with t.cuda.stream(side):
+        Kmod.acceptance_stats(dev, 7, retention_step=3)
+    t.cuda.current_stream().wait_stream(side)
+    t.cuda.synchronize()
+    g = t.cuda.CUDAGraph()
+    with t.cuda.graph(g):
+        outs = Kmod.acceptance_stats(dev, 7, retention_step=3)
+    for rep in range(4):
+        for x in outs:
+            x.zero_()
+        t.cuda.synchronize()
+        g.replay()
+        t.cuda.synchronize()
+        for x, e in zip(outs, eager):
+            assert t.equal(x, e), rep
+        Kmod.acceptance_stats(dev, 7, retention_step=3)   # eager work between replays
+        t.cuda.synchronize()
+    assert np.array_equal(eager[0].cpu().numpy(), oracle.acceptance_counts(acc, 7))
+
+
 @pytest.mark.parametrize("method", ["Proj + RoPE fix", "Gated KV (ckpt)"])
 def test_ten_million_verifications_of_a_printed_row(method):
     row = [r for r in GOLDEN["rows"] if r["method"] == method][0]
