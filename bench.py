@@ -25,33 +25,46 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+import workloads.device as WD  # noqa: E402  (seeded inputs only)
+
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 METRIC = "draft-attention effective HBM GB/s (% of peak) + draft tokens/s at 32K ctx"
 DEFAULT_WORKLOAD = "long_b64_ctx32k_k8"
+# bf16 parity bars against the float64 oracle (the parity sample must meet both)
+PARITY_MAX_ABS = 2e-2
+PARITY_REL_L2 = 5e-3
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+KERNEL_SOURCES = {1: ("attn_mfma.hip", "attn_mfma_common.h", "kvshot_common.h"),
+                  3: ("attn_tall.hip", "attn_mfma_common.h", "kvshot_common.h")}
+KERNEL_NAMES = {1: "attn_mfma_kernel", 2: "attn_generic_kernel", 3: "attn_tall_kernel"}
+PROFILE_PREFIX = {1: "attn_mfma", 3: "attn_tall"}
+
+
+def kernel_source_hash(path: int = 1) -> str:
     h = hashlib.sha256()
-    for f in ("attn_mfma.hip", "kvshot_common.h"):
+    for f in KERNEL_SOURCES[path]:
         h.update(open(os.path.join(ROOT, "paper_2604_26412_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str, mode: str):
+def read_traffic(workload: str, mode: str, kernel_path: int = 1):
     """HBM bytes per attention launch from a committed counter summary, if it matches this kernel source."""
-    path = os.path.join(PROFILES, f"attn_mfma_{workload}_{mode}_counters.md")
+    if kernel_path not in PROFILE_PREFIX:
+        return None
+    path = os.path.join(PROFILES, f"{PROFILE_PREFIX[kernel_path]}_{workload}_{mode}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
     f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
     w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not (m and f and w) or m.group(1) != kernel_source_hash():
+    if not (m and f and w) or m.group(1) != kernel_source_hash(kernel_path):
         return None
     return float(f.group(1)) + float(w.group(1))
 
@@ -59,34 +72,6 @@ def read_traffic(workload: str, mode: str):
 # ---------------------------------------------------------------------------
 # workloads on the device
 # ---------------------------------------------------------------------------
-
-def make_long_range_on_device(torch, seed, B=64, T=32768, n=8, Hq=32, Hkv=8, D=128, P=16, contiguous=False):
-    """Seeded device-side generator for the 64 x 32768 workload (values N(0,1), bf16, random page table;
-    ``contiguous``: sequence b owns pages b * T / P onward, in order)."""
-    g = torch.Generator(device="cuda")
-    g.manual_seed(seed)
-    pps = T // P
-    used = B * pps
-    pool = used + max(1, used // 100)
-    dev = "cuda"
-    kp = torch.randn((pool, Hkv, P, D), generator=g, device=dev, dtype=torch.bfloat16)
-    vp = torch.randn((pool, Hkv, P, D), generator=g, device=dev, dtype=torch.bfloat16)
-    perm = torch.randperm(pool, generator=g, device=dev)
-    if contiguous:
-        perm = torch.arange(pool, device=dev)
-    table = perm[:used].view(B, pps).to(torch.int32).contiguous()
-    spare = perm[used:]
-    kp[spare] = float("nan")
-    vp[spare] = float("nan")
-    q = torch.randn((B, n, Hq, D), generator=g, device=dev, dtype=torch.bfloat16)
-    dk = torch.randn((B, n, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-    dv = torch.randn((B, n, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-    lens = torch.full((B,), T, dtype=torch.int32, device=dev)
-    offs = torch.zeros((B,), dtype=torch.int32, device=dev)
-    return dict(mode="step", q=q, k_pages=kp, v_pages=vp, page_table=table, ctx_lens=lens, draft_k=dk, draft_v=dv,
-                extra=offs, pool=pool, pps=pps, B=B, n=n, Hq=Hq, Hkv=Hkv, D=D, P=P, max_draft=n,
-                lens=[T] * B, offsets=[0] * B, dtype="bf16", host=None, theta=1e6, scale=0.0)
-
 
 def upload_case(torch, case):
     import numpy as np
@@ -104,27 +89,6 @@ def upload_case(torch, case):
                 lens=[int(x) for x in case.ctx_lens], dtype=case.dtype, host=case, theta=case.rope_theta,
                 scale=case.softmax_scale,
                 offsets=[int(x) for x in case.step_offsets] if case.mode == "step" else [0] * B)
-
-
-def host_sample_long(torch, d, seqs):
-    """Copy sequences `seqs` of the device-generated workload into a compact host case (for the oracle)."""
-    import numpy as np
-
-    import workloads as W
-
-    def bits(t):
-        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-
-    table = d["page_table"][seqs].long()
-    ns, pps = table.shape
-    kp = bits(d["k_pages"][table.reshape(-1)])
-    vp = bits(d["v_pages"][table.reshape(-1)])
-    pt = np.arange(ns * pps, dtype=np.int32).reshape(ns, pps)
-    return W.DraftCase(mode="step", dtype="bf16", num_q_heads=d["Hq"], num_kv_heads=d["Hkv"], head_dim=d["D"],
-                       page_size=d["P"], max_draft=d["n"], n_new=d["n"], q=bits(d["q"][seqs]), k_pages=kp,
-                       v_pages=vp, page_table=pt, ctx_lens=np.array([d["lens"][s] for s in seqs], np.int32),
-                       draft_k=bits(d["draft_k"][seqs]), draft_v=bits(d["draft_v"][seqs]),
-                       step_offsets=np.zeros(ns, np.int32))
 
 
 # ---------------------------------------------------------------------------
@@ -173,7 +137,7 @@ def cpu_baseline(torch, d, out_gpu, budget_s=15.0):
 
     def sample(seqs):
         if d["host"] is None:
-            return host_sample_long(torch, d, seqs), None
+            return WD.host_sample(torch, d, seqs), None
         return d["host"], seqs
 
     c0, s0 = sample([0])
@@ -286,7 +250,7 @@ def main():
         raise SystemExit("fusion workloads run with --op fusion")
     if args.workload == DEFAULT_WORKLOAD:
         log("generating the 64 x 32768 workload on the device")
-        d = make_long_range_on_device(torch, args.seed, contiguous=args.contiguous)
+        d = WD.long_range_on_device(torch, args.seed, contiguous=args.contiguous)
     elif args.contiguous:
         raise SystemExit("--contiguous applies to the 64 x 32K workload only")
     else:
@@ -415,10 +379,10 @@ def main():
 
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     achieved = attn_launch_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = read_traffic(args.workload, args.mode) if not args.splits and plan["path"] == 1 else None
-    path_name = {1: "attn_mfma_kernel", 2: "attn_generic_kernel"}[plan["path"]]
+    traffic = read_traffic(args.workload, args.mode, plan["path"]) if not args.splits else None
+    path_name = KERNEL_NAMES[plan["path"]]
     kernel = f"{path_name} ({plan['row_tiles']} x 32-row query tiles per (sequence, KV head))" \
-        if plan["path"] == 1 else path_name
+        if plan["path"] != 2 else path_name
     res = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -441,7 +405,7 @@ def main():
                    "batch": B, "ctx_len_max": T_max, "draft_queries": n, "mode": args.mode if d["mode"] == "step"
                    else "tree", "page_size": P, "splits": plan["splits"], "workgroups": plan["workgroups"],
                    "cold_caches": bool(args.cold), "launch": "python" if args.no_graph else "hip graph replay",
-                   "path": {1: "mfma", 2: "generic"}[plan["path"]],
+                   "path": {1: "mfma", 2: "generic", 3: "mfma (tall tiles)"}[plan["path"]],
                    "page_table": "contiguous" if args.contiguous else "random permutation"},
         "call_ms": call_ms,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -456,9 +420,14 @@ def main():
         log("timing the CPU oracle on a bounded sample")
         cb, parity = cpu_baseline(torch, d, out)
         res["cpu_baseline"] = cb
+        parity["ok"] = parity["max_abs"] <= PARITY_MAX_ABS and parity["rel_l2"] <= PARITY_REL_L2
         res["parity_sample"] = parity
     print(json.dumps(res), flush=True)
     att.close()
+    if "parity_sample" in res and not res["parity_sample"]["ok"]:
+        log(f"parity sample misses the bars (max-abs <= {PARITY_MAX_ABS}, rel-L2 <= {PARITY_REL_L2}): "
+            f"{res['parity_sample']}")
+        sys.exit(1)
 
 
 # ---------------------------------------------------------------------------

@@ -21,7 +21,7 @@ LIB_NAME = "libkvshot_draft_attn.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "attn_mfma.hip", "attn_generic.hip", "combine.hip", "debug.hip", "fusion.hip", "fusion_api.cpp", "kvproj.hip", "kvproj_api.cpp", "metrics.hip", "tree_grow.hip"]
+SOURCES = ["api.cpp", "attn_mfma.hip", "attn_tall.hip", "attn_generic.hip", "combine.hip", "debug.hip", "fusion.hip", "fusion_api.cpp", "kvproj.hip", "kvproj_api.cpp", "metrics.hip", "tree_grow.hip"]
 
 COMMON_FLAGS = [
     "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",

@@ -13,6 +13,7 @@
 #include <new>
 #include <vector>
 
+#include "device_guard.h"
 #include "kvshot_common.h"
 
 using namespace kvshot;
@@ -65,12 +66,23 @@ struct Plan {
   int waves_per_wg;
 };
 
+// 32-row tiles from which the tall-tile kernel serves a call
+constexpr int kTallRowTiles = 8;
+
+bool use_tall_kernel() {
+#ifdef KVSHOT_NO_TALL
+  return false;
+#else
+  return true;
+#endif
+}
+
 int round_tiles(int rows) {
   const int t = (rows + 31) / 32;
   return t <= 1 ? 1 : (t <= 2 ? 2 : (t <= 4 ? 4 : 8));
 }
 
-Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
+Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_tall = true) {
   Plan pl{};
   pl.rows = c->group * nq;
   const bool generic = c->cfg.dtype == KVSHOT_FP32 || c->opt_path == 2;
@@ -81,6 +93,13 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
     pl.kernel_row_tiles = pl.row_tiles;
     pl.row_groups = 1;
     pl.waves_per_wg = 4;
+    pl.key_streams = 1;
+  } else if (pl.row_tiles >= kTallRowTiles && allow_tall && use_tall_kernel()) {
+    // 256-row tiles (draft trees, 33..64 queries at G = 4): the tall-tile kernel
+    pl.path = 3;
+    pl.kernel_row_tiles = tall_waves_per_wg();
+    pl.row_groups = pl.row_tiles / pl.kernel_row_tiles;
+    pl.waves_per_wg = tall_waves_per_wg();
     pl.key_streams = 1;
   } else {
     pl.kernel_row_tiles = mfma_kernel_row_tiles(pl.row_tiles);
@@ -99,13 +118,15 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
     // blocks per wave.  (Each workgroup starts with a dependent chain of
     // loads -- length, page ids, K/V, RoPE table -- that only other resident
     // workgroups can hide, so more, shorter workgroups lose.)
-    const int per_cu = generic ? 2 : mfma_wgs_per_cu(pl.kernel_row_tiles);
+    const int per_cu = generic ? 2 : (pl.path == 3 ? 8 / pl.waves_per_wg : mfma_wgs_per_cu(pl.kernel_row_tiles));
     const int target_wgs = c->num_cus * per_cu;
     splits = (target_wgs + pairs - 1) / pairs;
     const int cap = nb / (pl.key_streams * 4);
     splits = splits > cap ? cap : splits;
   }
   if (splits < 1) splits = 1;
+  // the tall-tile kernel stages a split's page ids in LDS: at most tall_max_blocks() blocks per split
+  if (pl.path == 3 && nb > (int64_t)splits * tall_max_blocks()) splits = (nb + tall_max_blocks() - 1) / tall_max_blocks();
   if (splits > c->max_splits) splits = c->max_splits;
   // the workspace must hold this call's partials
   while (splits > 1 && (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * splits > c->ws_rows) --splits;
@@ -113,16 +134,12 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx) {
   bps = ((bps + pl.key_streams - 1) / pl.key_streams) * pl.key_streams;
   if (bps > 0) splits = (nb + bps - 1) / bps;
   if (splits < 1) splits = 1;
+  // more blocks per split than the tall-tile kernel stages (contexts beyond what the split cap
+  // covers, or a forced split count): the general kernel serves the call
+  if (pl.path == 3 && bps > tall_max_blocks()) return make_plan(c, batch, nq, max_ctx, false);
   pl.splits = splits;
   pl.blocks_per_split = bps;
   return pl;
-}
-
-kvshot_status check_device(const kvshot_ctx* c) {
-  int cur = -1;
-  if (hipGetDevice(&cur) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  if (cur != c->device && hipSetDevice(c->device) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  return KVSHOT_OK;
 }
 
 void fill_params(const kvshot_ctx* c, const Plan& pl, int batch, int nq, int max_ctx, AttnParams& p) {
@@ -193,8 +210,9 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
       !aligned16(a.draft_v) || !aligned16(a.out))
     return KVSHOT_ERR_INVALID_ARG;
   if (c->opt_path == 1 && g.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
-  kvshot_status st = check_device(c);
-  if (st != KVSHOT_OK) return st;
+  const DeviceGuard dg(c->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
+  kvshot_status st = KVSHOT_OK;
 
   const Plan pl = make_plan(c, batch, nq, max_ctx);
   AttnParams p;
@@ -234,8 +252,9 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
     slot = &c->prof[c->prof_head % kProfileRing];
     if (hipEventRecord(slot->ev[0], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   }
-  hipError_t e = pl.path == 1 ? launch_attn_mfma(p, pl.kernel_row_tiles, s)
-                              : launch_attn_generic(p, g.dtype == KVSHOT_BF16, s);
+  hipError_t e = pl.path == 1   ? launch_attn_mfma(p, pl.kernel_row_tiles, s)
+                 : pl.path == 3 ? launch_attn_tall(p, s)
+                                : launch_attn_generic(p, g.dtype == KVSHOT_BF16, s);
   if (e != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (slot && hipEventRecord(slot->ev[1], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (pl.splits > 1) {
@@ -274,8 +293,9 @@ kvshot_status validate_impl(kvshot_ctx* c, const kvshot_call& a, int32_t* first_
   if (tree && (a.n_nodes < 1 || a.n_nodes > g.max_draft)) return KVSHOT_ERR_INVALID_ARG;
   if (a.max_ctx_len_hint < 0 || (int64_t)a.max_ctx_len_hint > (int64_t)g.max_pages_per_seq * g.page_size)
     return KVSHOT_ERR_INVALID_ARG;
-  kvshot_status st = check_device(c);
-  if (st != KVSHOT_OK) return st;
+  const DeviceGuard dg(c->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
+  kvshot_status st = KVSHOT_OK;
   const Plan pl = make_plan(c, a.batch, a.n_queries, a.max_ctx_len_hint);
   AttnParams p;
   fill_params(c, pl, a.batch, a.n_queries, a.max_ctx_len_hint, p);
@@ -299,7 +319,7 @@ kvshot_status validate_impl(kvshot_ctx* c, const kvshot_call& a, int32_t* first_
 
 void free_ctx(kvshot_ctx* c) {
   if (!c) return;
-  (void)hipSetDevice(c->device);
+  const DeviceGuard dg(c->device);
   (void)hipDeviceSynchronize();
   if (c->rope) (void)hipFree(c->rope);
   if (c->part_o) (void)hipFree(c->part_o);
@@ -495,7 +515,8 @@ kvshot_status kvshot_draft_attn_set_option(kvshot_handle h, int32_t option, int6
     case KVSHOT_OPT_PROFILE:
       if (value != 0 && value != 1) return KVSHOT_ERR_INVALID_ARG;
       if (value && h->prof.empty()) {
-        if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+        const DeviceGuard dg(h->device);
+        if (!dg.ok()) return KVSHOT_ERR_DEVICE;
         h->prof.resize(kProfileRing);
         for (auto& s : h->prof) {
           for (auto& e : s.ev) {
@@ -527,7 +548,8 @@ kvshot_status kvshot_draft_attn_plan(kvshot_handle h, int32_t batch, int32_t n_q
 
 kvshot_status kvshot_draft_attn_profile_read(kvshot_handle h, double* attn_ms, double* combine_ms, int64_t* calls) {
   if (!h) return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   kvshot_status st = drain_profile(h, true);
   if (st != KVSHOT_OK) return st;
   if (attn_ms) *attn_ms = h->attn_ms;
@@ -545,8 +567,9 @@ kvshot_status kvshot_debug_gather_kv(kvshot_handle h, int32_t batch, int32_t max
   if (batch < 1 || batch > h->cfg.max_batch || max_ctx < 1) return KVSHOT_ERR_INVALID_ARG;
   if (!aligned16(k_pages) || !aligned16(v_pages) || !aligned16(k_dense) || !aligned16(v_dense))
     return KVSHOT_ERR_INVALID_ARG;
-  kvshot_status st = check_device(h);
-  if (st != KVSHOT_OK) return st;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
+  kvshot_status st = KVSHOT_OK;
   const Plan pl = make_plan(h, batch, 1, 0);
   AttnParams p;
   fill_params(h, pl, batch, 1, max_ctx, p);
@@ -563,8 +586,9 @@ kvshot_status kvshot_debug_tree_mask(kvshot_handle h, int32_t batch, int32_t n_n
                                      uint64_t* anc_out, int32_t* depth_out, void* stream) {
   if (!h || !parents || !anc_out || !depth_out) return KVSHOT_ERR_INVALID_ARG;
   if (batch < 1 || batch > h->cfg.max_batch || n_nodes < 1 || n_nodes > kMaxDraft) return KVSHOT_ERR_INVALID_ARG;
-  kvshot_status st = check_device(h);
-  if (st != KVSHOT_OK) return st;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
+  kvshot_status st = KVSHOT_OK;
   if (launch_tree_mask(parents, batch, n_nodes, anc_out, depth_out, (hipStream_t)stream) != hipSuccess)
     return KVSHOT_ERR_DEVICE;
   return KVSHOT_OK;

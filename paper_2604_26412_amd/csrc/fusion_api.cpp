@@ -9,6 +9,7 @@
 #include <new>
 #include <vector>
 
+#include "device_guard.h"
 #include "fusion_common.h"
 
 using namespace kvshot;
@@ -58,22 +59,15 @@ int plan_splits(const kvshot_fusion_ctx* c, int tokens) {
 
 void free_fusion(kvshot_fusion_ctx* c) {
   if (!c) return;
-  int cur = -1;
-  if (hipGetDevice(&cur) == hipSuccess && cur != c->device) (void)hipSetDevice(c->device);
-  (void)hipDeviceSynchronize();
-  for (auto& s : c->prof)
-    for (auto& e : s.ev)
-      if (e) (void)hipEventDestroy(e);
-  if (c->part) (void)hipFree(c->part);
-  if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
+  {
+    const DeviceGuard dg(c->device);
+    (void)hipDeviceSynchronize();
+    for (auto& s : c->prof)
+      for (auto& e : s.ev)
+        if (e) (void)hipEventDestroy(e);
+    if (c->part) (void)hipFree(c->part);
+  }
   delete c;
-}
-
-kvshot_status check_device(const kvshot_fusion_ctx* c) {
-  int cur = -1;
-  if (hipGetDevice(&cur) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  if (cur != c->device && hipSetDevice(c->device) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  return KVSHOT_OK;
 }
 
 kvshot_status drain_profile(kvshot_fusion_ctx* c, bool all) {
@@ -103,7 +97,8 @@ kvshot_status run_fusion(kvshot_fusion_handle h, int32_t tokens, const void* n, 
   if ((n && !aligned16(n)) || !aligned16(o) || !aligned16(b_g) || !aligned16(h_out) || (g_out && !aligned16(g_out)) ||
       (packed && !aligned16(packed)) || (w_g && !aligned16(w_g)) || (w_delta && !aligned16(w_delta)))
     return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
 
   FusionParams p{};
   p.n = (const uint16_t*)n;
@@ -210,7 +205,8 @@ kvshot_status kvshot_fusion_pack_weights(kvshot_fusion_handle h, const void* w_g
                                          void* stream) {
   if (!h || !w_g || !w_delta || !packed) return KVSHOT_ERR_INVALID_ARG;
   if (!aligned16(w_g) || !aligned16(w_delta) || !aligned16(packed)) return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   if (launch_fusion_pack((const uint16_t*)w_g, (const uint16_t*)w_delta, (uint16_t*)packed, h->d,
                          (hipStream_t)stream) != hipSuccess)
     return KVSHOT_ERR_DEVICE;
@@ -235,7 +231,8 @@ kvshot_status kvshot_fusion_set_option(kvshot_fusion_handle h, int32_t option, i
     case KVSHOT_OPT_PROFILE:
       if (value != 0 && value != 1) return KVSHOT_ERR_INVALID_ARG;
       if (value && h->prof.empty()) {
-        if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+        const DeviceGuard dg(h->device);
+        if (!dg.ok()) return KVSHOT_ERR_DEVICE;
         h->prof.resize(kFusionProfileRing);
         for (auto& sl : h->prof) {
           for (auto& e : sl.ev) {
@@ -263,7 +260,8 @@ kvshot_status kvshot_fusion_plan(kvshot_fusion_handle h, int32_t tokens, int32_t
 kvshot_status kvshot_fusion_profile_read(kvshot_fusion_handle h, double* main_ms, double* combine_ms,
                                          int64_t* calls) {
   if (!h) return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   const kvshot_status st = drain_profile(h, true);
   if (st != KVSHOT_OK) return st;
   if (main_ms) *main_ms = h->main_ms;

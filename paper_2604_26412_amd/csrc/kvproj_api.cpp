@@ -11,6 +11,7 @@
 #include <new>
 #include <vector>
 
+#include "device_guard.h"
 #include "kvproj_common.h"
 
 using namespace kvshot;
@@ -66,25 +67,18 @@ int plan_splits(const kvshot_kvproj_ctx* c, int n_tokens) {
 
 void free_proj(kvshot_kvproj_ctx* c) {
   if (!c) return;
-  int cur = -1;
-  if (hipGetDevice(&cur) == hipSuccess && cur != c->device) (void)hipSetDevice(c->device);
-  (void)hipDeviceSynchronize();
-  for (auto& s : c->prof)
-    for (auto& e : s.ev)
-      if (e) (void)hipEventDestroy(e);
-  if (c->rope) (void)hipFree(c->rope);
-  if (c->rope_rev) (void)hipFree(c->rope_rev);
-  if (c->part) (void)hipFree(c->part);
-  if (c->flag) (void)hipFree(c->flag);
-  if (cur >= 0 && cur != c->device) (void)hipSetDevice(cur);
+  {
+    const DeviceGuard dg(c->device);
+    (void)hipDeviceSynchronize();
+    for (auto& s : c->prof)
+      for (auto& e : s.ev)
+        if (e) (void)hipEventDestroy(e);
+    if (c->rope) (void)hipFree(c->rope);
+    if (c->rope_rev) (void)hipFree(c->rope_rev);
+    if (c->part) (void)hipFree(c->part);
+    if (c->flag) (void)hipFree(c->flag);
+  }
   delete c;
-}
-
-kvshot_status check_device(const kvshot_kvproj_ctx* c) {
-  int cur = -1;
-  if (hipGetDevice(&cur) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  if (cur != c->device && hipSetDevice(c->device) != hipSuccess) return KVSHOT_ERR_DEVICE;
-  return KVSHOT_OK;
 }
 
 kvshot_status drain_profile(kvshot_kvproj_ctx* c, bool all) {
@@ -241,7 +235,8 @@ kvshot_status kvshot_kv_project(kvshot_kvproj_handle h, int32_t n_tokens, int32_
     p.v_src[l] = p.v_src[0];
   }
   if (!aligned16(w_k) || !aligned16(w_v) || !aligned16(k_dst) || !aligned16(v_dst)) return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   p.w_k = (const uint16_t*)w_k;
   p.w_v = (const uint16_t*)w_v;
   p.k_dst = (uint16_t*)k_dst;
@@ -278,7 +273,8 @@ kvshot_status kvshot_kv_project_validate(kvshot_kvproj_handle h, int32_t n_token
   KvProjParams p;
   const kvshot_status st = base_params(h, n_tokens, batch, page_table, token_seq, token_pos, dst_page_table, &p);
   if (st != KVSHOT_OK) return st;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   hipStream_t s = (hipStream_t)stream;
   if (launch_kvproj_validate(p, h->flag, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   int32_t v = 0;
@@ -305,7 +301,8 @@ kvshot_status kvshot_kvproj_set_option(kvshot_kvproj_handle h, int32_t option, i
     case KVSHOT_OPT_PROFILE:
       if (value != 0 && value != 1) return KVSHOT_ERR_INVALID_ARG;
       if (value && h->prof.empty()) {
-        if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+        const DeviceGuard dg(h->device);
+        if (!dg.ok()) return KVSHOT_ERR_DEVICE;
         h->prof.resize(kProjProfileRing);
         for (auto& sl : h->prof) {
           for (auto& e : sl.ev) {
@@ -333,7 +330,8 @@ kvshot_status kvshot_kvproj_plan(kvshot_kvproj_handle h, int32_t n_tokens, int32
 kvshot_status kvshot_kvproj_profile_read(kvshot_kvproj_handle h, double* main_ms, double* combine_ms,
                                          int64_t* calls) {
   if (!h) return KVSHOT_ERR_INVALID_ARG;
-  if (check_device(h) != KVSHOT_OK) return KVSHOT_ERR_DEVICE;
+  const DeviceGuard dg(h->device);
+  if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   const kvshot_status st = drain_profile(h, true);
   if (st != KVSHOT_OK) return st;
   if (main_ms) *main_ms = h->main_ms;

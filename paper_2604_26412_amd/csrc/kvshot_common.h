@@ -160,6 +160,9 @@ __device__ __forceinline__ uint64_t tree_ancestry_wave(const int32_t* parents_ro
 // Launchers (defined in the .hip files).
 namespace kvshot {
 hipError_t launch_attn_mfma(const AttnParams& p, int kernel_row_tiles, hipStream_t s);
+hipError_t launch_attn_tall(const AttnParams& p, hipStream_t s);
+int tall_waves_per_wg();
+int tall_max_blocks();
 hipError_t launch_attn_generic(const AttnParams& p, int bf16_in, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_gather_kv(const AttnParams& p, int max_ctx, void* k_dense, void* v_dense, int bf16, hipStream_t s);

@@ -139,6 +139,92 @@ def test_tree_b8_ctx16k_n60():
 
 
 # ---------------------------------------------------------------------------
+# the 64 x 32768 workload the headline metric is quoted on (generated on the
+# device; whole sampled sequences are copied back for the oracle)
+# ---------------------------------------------------------------------------
+
+LONG_SAMPLE = [0, 21, 42, 63]          # first, two interior, last
+
+
+@pytest.fixture(scope="module")
+def long_range():
+    import torch
+
+    import workloads.device as WD
+    _log("generating the 64 x 32768 workload on the device")
+    d = WD.long_range_on_device(torch, 1004)
+    torch.cuda.synchronize()
+    # the pool holds more than 2^31 elements per tensor, so 32-bit element offsets would wrap
+    assert d["k_pages"].numel() > 2 ** 31
+    host = WD.host_sample(torch, d, LONG_SAMPLE)
+    ref, ref_lse = G.oracle_out(host)
+    yield d, host, ref, ref_lse
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("sequential", [False, True])
+def test_long_b64_ctx32k_k8(long_range, sequential):
+    """Whole batch on the GPU in the bench's launch configuration (automatic plan); four whole
+    sequences checked element by element, LSE included."""
+    import torch
+
+    from paper_2604_26412_amd import DraftAttention
+    d, host, ref, ref_lse = long_range
+    B, n, Hq, D = d["B"], d["n"], d["Hq"], d["D"]
+    T = d["lens"][0]
+    out = torch.empty((B, n, Hq, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((B, n, Hq), dtype=torch.float32, device="cuda")
+    with DraftAttention(num_q_heads=Hq, num_kv_heads=d["Hkv"], head_dim=D, page_size=d["P"], dtype="bf16",
+                        max_batch=B, max_draft=d["max_draft"], max_pages_per_seq=d["pps"],
+                        num_pages=d["pool"]) as att:
+        _log(f"64 x 32K sequential={sequential}: plan {att.plan(B, 1 if sequential else n, T)}")
+        if not sequential:
+            att.step(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["ctx_lens"], d["draft_k"],
+                     d["draft_v"], d["extra"], max_ctx=T, out=out, lse=lse)
+        else:
+            for j in range(n):
+                oj = torch.empty((B, 1, Hq, D), dtype=torch.bfloat16, device="cuda")
+                lj = torch.empty((B, 1, Hq), dtype=torch.float32, device="cuda")
+                att.step(d["q"][:, j:j + 1].contiguous(), d["k_pages"], d["v_pages"], d["page_table"],
+                         d["ctx_lens"], d["draft_k"], d["draft_v"], (d["extra"] + j).contiguous(), max_ctx=T,
+                         out=oj, lse=lj)
+                out[:, j:j + 1] = oj
+                lse[:, j:j + 1] = lj
+        torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all(), "non-finite output in the unsampled sequences"
+    got = out[LONG_SAMPLE].float().cpu().numpy().astype(np.float64)
+    got_lse = lse[LONG_SAMPLE].cpu().numpy().astype(np.float64)
+    mx, rel = G.assert_parity(got, ref, "bf16", f"64 x 32K sequential={sequential}")
+    worst = float((np.abs(got_lse - ref_lse) / G.lse_tolerance(host)).max())
+    assert worst <= 1.0, f"lse error exceeds its bound by {worst:.2f}x"
+    _log(f"64 x 32K sequential={sequential}: max_abs {mx:.3e} rel_l2 {rel:.3e} lse/bound {worst:.3f}")
+
+
+# ---------------------------------------------------------------------------
+# tall query tiles (more than 32 rows per (sequence, KV head)) on outlier keys:
+# the recipe of the single-sequence workload (4 channels per KV head x 8) and
+# a heavier one (2 channels x 32), which make scores sensitive to the query's
+# rounding
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("outliers", [(4, 8.0), (2, 32.0)])
+@pytest.mark.parametrize("n_new", [9, 16, 33, 64])
+def test_tall_tiles_outlier_keys(n_new, outliers):
+    no, sc = outliers
+    c = small(n_new=n_new, max_draft=64, ctx_lens=[4096, 1500, 0], n_outlier=no, outlier_scale=sc,
+              seed=151 + n_new)
+    _check_case(c, what=f"tall tile n_new={n_new} outliers {no}x{sc:g}")
+
+
+@pytest.mark.parametrize("outliers", [(4, 8.0), (2, 32.0)])
+def test_tree_b8_ctx16k_n60_outlier_keys(outliers):
+    no, sc = outliers
+    c = W.workload("tree_b8_ctx16k_n60", n_outlier=no, outlier_scale=sc)
+    _check_case(c, what=f"tree b8 ctx16k n60 outliers {no}x{sc:g}")
+
+
+# ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
 

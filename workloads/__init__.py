@@ -215,7 +215,7 @@ def make_case(*, mode: str = "step", batch: int = 1, ctx_lens=None, n_new: int =
               num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128, page_size: int = 16,
               dtype: str = "bf16", seed: int = 0, max_draft: Optional[int] = None, step_offsets=None,
               parents=None, shuffle: bool = True, poison: bool = True, n_outlier: int = 0,
-              rope_theta: float = 1e6, softmax_scale: float = 0.0, name: str = "",
+              outlier_scale: float = 8.0, rope_theta: float = 1e6, softmax_scale: float = 0.0, name: str = "",
               max_pages_per_seq: Optional[int] = None) -> DraftCase:
     if ctx_lens is None:
         ctx_lens = [256] * batch
@@ -237,7 +237,7 @@ def make_case(*, mode: str = "step", batch: int = 1, ctx_lens=None, n_new: int =
         raise ValueError("max_draft too small")
     k_pages, v_pages, page_table = build_pages(seed, ctx_lens, num_kv_heads, head_dim, page_size, dtype,
                                                shuffle=shuffle, poison=poison, n_outlier=n_outlier,
-                                               max_pages_per_seq=max_pages_per_seq)
+                                               outlier_scale=outlier_scale, max_pages_per_seq=max_pages_per_seq)
     q = _encode(_normal(seed, _TID_Q, (B, n_new, num_q_heads, head_dim)), dtype)
     dk = _encode(_normal(seed, _TID_DK, (B, max_draft, num_kv_heads, head_dim)), dtype)
     dv = _encode(_normal(seed, _TID_DV, (B, max_draft, num_kv_heads, head_dim)), dtype)
