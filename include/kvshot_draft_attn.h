@@ -52,7 +52,8 @@ typedef enum {
   KVSHOT_ERR_UNSUPPORTED = 2,   /* valid but not implemented (head_dim != 128, ...) */
   KVSHOT_ERR_OUT_OF_MEMORY = 3, /* device allocation in init failed */
   KVSHOT_ERR_DEVICE = 4,        /* a HIP call or kernel launch failed */
-  KVSHOT_ERR_DATA = 5           /* validate found a contract violation in device data */
+  KVSHOT_ERR_DATA = 5,          /* validate found a contract violation in device data */
+  KVSHOT_ERR_SCRATCH = 6        /* kvshot_draft_attn_call_noalloc: the call needs more scratch than it has */
 } kvshot_status;
 
 typedef enum { KVSHOT_BF16 = 0, KVSHOT_FP32 = 1 } kvshot_dtype;
@@ -171,6 +172,25 @@ typedef struct kvshot_call {
 
 /* Runs the call described by *call (host struct; device pointers inside). */
 kvshot_status kvshot_draft_attn_call(kvshot_handle h, const kvshot_call* call, void* stream);
+
+/* kvshot_draft_attn_call for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, plan, kernels and result bits as
+ * kvshot_draft_attn_call; the difference is where the split-K partials go:
+ * a 32 MiB array in the library's static device memory (one copy per GPU,
+ * held until the process ends; its address is resolved once per device by
+ * kvshot_draft_attn_init), instead of the handle's workspace.  The call
+ * allocates nothing and records no profiling events.
+ *   - A call whose partials exceed 32 MiB (batch x num_kv_heads x padded rows
+ *     x splits x (128 x 4 + 8) bytes, the partial (m, l) rows aligned to 256
+ *     bytes; a one-split plan needs none) returns KVSHOT_ERR_SCRATCH and
+ *     queues nothing.
+ *   - Every call on one GPU shares that GPU's scratch: calls that overlap in
+ *     time on one GPU (from any handle, stream or thread) race and give
+ *     undefined results.  Calls ordered on one stream are safe.
+ *   - The scratch keeps the last call's contents; nothing in it needs to start
+ *     at zero (every partial a call reads is written earlier in the call). */
+kvshot_status kvshot_draft_attn_call_noalloc(kvshot_handle h, const kvshot_call* call, void* stream);
 
 /* kvshot_draft_attn_validate for a kvshot_call: also checks query_nodes
  * (code 5: a node outside [0, n_nodes)) and pos_base (code 6: negative, or a

@@ -20,7 +20,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvshot_draft_attn.so")
 
 KVSHOT_OK = 0
-STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_MEMORY", 4: "DEVICE", 5: "DATA"}
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_MEMORY", 4: "DEVICE", 5: "DATA",
+                6: "SCRATCH"}
 BF16, FP32 = 0, 1
 OPT_SPLITS, OPT_PATH, OPT_PROFILE = 0, 1, 2
 
@@ -28,7 +29,8 @@ EXPORTED_SYMBOLS = [
     "kvshot_draft_attn_init", "kvshot_draft_attn_destroy", "kvshot_draft_attn_step", "kvshot_draft_attn_tree",
     "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
     "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_debug_stream_read",
-    "kvshot_status_string", "kvshot_draft_attn_call", "kvshot_draft_attn_validate_call",
+    "kvshot_status_string", "kvshot_draft_attn_call", "kvshot_draft_attn_call_noalloc",
+    "kvshot_draft_attn_validate_call",
     "kvshot_fusion_init", "kvshot_fusion_destroy", "kvshot_gated_delta_fusion", "kvshot_fusion_set_option",
     "kvshot_fusion_plan", "kvshot_fusion_profile_read", "kvshot_fusion_pack_weights",
     "kvshot_gated_delta_fusion_packed",
@@ -113,6 +115,7 @@ def load_library(path: Optional[str] = None):
         "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
         "kvshot_debug_stream_read": [_vp, _i64, _vp, _i32, _vp],
         "kvshot_draft_attn_call": [_vp, ctypes.POINTER(KvshotCall), _vp],
+        "kvshot_draft_attn_call_noalloc": [_vp, ctypes.POINTER(KvshotCall), _vp],
         "kvshot_draft_attn_validate_call": [_vp, ctypes.POINTER(KvshotCall), ctypes.POINTER(_i32), _vp],
         "kvshot_fusion_init": [_i32, _i32, ctypes.POINTER(_vp)],
         "kvshot_fusion_destroy": [_vp],
@@ -285,41 +288,46 @@ class DraftAttention:
 
     # -- calls -------------------------------------------------------------
     def step(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, step_offsets, *, max_ctx=None,
-             out=None, lse=None, pos_base=None, stream=None):
+             out=None, lse=None, pos_base=None, stream=None, noalloc=False):
         """Causal draft steps; returns ``out`` [B][n_new][Hq][D].
 
         ``pos_base`` (int32 [B]) places draft step 0 of sequence b at position pos_base[b] instead of
-        ctx_lens[b] (see ``kvshot_call`` in the header).
+        ctx_lens[b] (see ``kvshot_call`` in the header).  ``noalloc`` calls
+        ``kvshot_draft_attn_call_noalloc`` (split partials in the library's static scratch).
         """
         torch = _torch()
         ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
         B = q.shape[0]
         offs = self._tensor(step_offsets, "step_offsets", torch.int32, (B,))
-        if pos_base is None:
+        if pos_base is None and not noalloc:
             _check("kvshot_draft_attn_step", self._lib.kvshot_draft_attn_step(
                 self._h, B, q.shape[1], self._hint(max_ctx), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["pt"],
                 ptrs["lens"], ptrs["dk"], ptrs["dv"], offs, ptrs["out"], ptrs["lse"], self._stream(stream)))
             return out
         call = self._call(MODE_STEP, q, q.shape[1], 0, max_ctx, ptrs, pos_base)
         call.step_offsets = offs
-        _check("kvshot_draft_attn_call", self._lib.kvshot_draft_attn_call(self._h, ctypes.byref(call),
-                                                                         self._stream(stream)))
+        self._run_call(call, stream, noalloc)
         return out
 
+    def _run_call(self, call, stream, noalloc):
+        name = "kvshot_draft_attn_call_noalloc" if noalloc else "kvshot_draft_attn_call"
+        _check(name, getattr(self._lib, name)(self._h, ctypes.byref(call), self._stream(stream)))
+
     def tree(self, q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, parents, *, max_ctx=None,
-             out=None, lse=None, query_nodes=None, pos_base=None, stream=None):
+             out=None, lse=None, query_nodes=None, pos_base=None, stream=None, noalloc=False):
         """Draft-tree queries with an ancestor-or-self mask; returns ``out`` [B][n_queries][Hq][D].
 
         ``parents`` is [B][n_nodes]; without ``query_nodes`` every node has a query row (n_queries ==
         n_nodes).  ``query_nodes`` (int32 [B][n_queries]) names the node of each query row, so a tree grown
-        level by level needs queries for its newest level only.  ``pos_base`` as in :meth:`step`.
+        level by level needs queries for its newest level only.  ``pos_base`` and ``noalloc`` as in
+        :meth:`step`.
         """
         torch = _torch()
         ptrs, out = self._common(q, k_pages, v_pages, page_table, ctx_lens, draft_k, draft_v, out, lse)
         B, nq = q.shape[0], q.shape[1]
         n_nodes = parents.shape[1] if parents.dim() == 2 else -1
         par = self._tensor(parents, "parents", torch.int32, (B, n_nodes))
-        if query_nodes is None and pos_base is None:
+        if query_nodes is None and pos_base is None and not noalloc:
             if n_nodes != nq:
                 raise ValueError("parents must be [B][n_queries] without query_nodes")
             _check("kvshot_draft_attn_tree", self._lib.kvshot_draft_attn_tree(
@@ -330,8 +338,7 @@ class DraftAttention:
         call.parents = par
         if query_nodes is not None:
             call.query_nodes = self._tensor(query_nodes, "query_nodes", torch.int32, (B, nq))
-        _check("kvshot_draft_attn_call", self._lib.kvshot_draft_attn_call(self._h, ctypes.byref(call),
-                                                                         self._stream(stream)))
+        self._run_call(call, stream, noalloc)
         return out
 
     def _call(self, mode, q, nq, n_nodes, max_ctx, ptrs, pos_base):

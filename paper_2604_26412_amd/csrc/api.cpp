@@ -10,6 +10,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -189,7 +190,16 @@ kvshot_status drain_profile(kvshot_ctx* c, bool all) {
   return KVSHOT_OK;
 }
 
-kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
+// Workspace of one call: where the split partials go, and whether profiling events may be recorded.
+struct Workspace {
+  float* part_o;
+  float2* part_ml;
+  bool profile;
+};
+
+kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const Workspace* ws = nullptr);
+
+kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const Workspace* ws) {
   if (!c) return KVSHOT_ERR_INVALID_ARG;
   const kvshot_config& g = c->cfg;
   const bool tree = a.mode == KVSHOT_MODE_TREE;
@@ -217,6 +227,10 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
   const Plan pl = make_plan(c, batch, nq, max_ctx);
   AttnParams p;
   fill_params(c, pl, batch, nq, max_ctx, p);
+  if (ws) {
+    p.part_o = ws->part_o;
+    p.part_ml = ws->part_ml;
+  }
   p.q = a.q;
   p.k_pages = a.k_pages;
   p.v_pages = a.v_pages;
@@ -237,7 +251,7 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
 
   ProfileSlot* slot = nullptr;
-  if (c->opt_profile) {
+  if (c->opt_profile && (!ws || ws->profile)) {
     if (c->prof_head - c->prof_tail >= kProfileRing) {
       st = drain_profile(c, false);
       if (st != KVSHOT_OK) return st;
@@ -259,8 +273,8 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream) {
   if (slot && hipEventRecord(slot->ev[1], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (pl.splits > 1) {
     CombineParams cp;
-    cp.part_o = c->part_o;
-    cp.part_ml = c->part_ml;
+    cp.part_o = p.part_o;
+    cp.part_ml = p.part_ml;
     cp.out = out;
     cp.lse = lse;
     cp.batch = batch;
@@ -317,6 +331,51 @@ kvshot_status validate_impl(kvshot_ctx* c, const kvshot_call& a, int32_t* first_
   return KVSHOT_ERR_DATA;
 }
 
+// ---------------------------------------------------------------------------
+// Static scratch for kvshot_draft_attn_call_noalloc: the split partials of a
+// call that may not allocate.  One copy per GPU, held until the process ends.
+// Its device address is resolved once per device (with that device current)
+// and kept; host code uses that address, never the array's name.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Resolve this device's scratch address (the device is current).  Idempotent.
+kvshot_status resolve_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return KVSHOT_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[device]) return KVSHOT_OK;
+  void* ptr = nullptr;
+  if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+    (void)hipGetLastError();
+    return KVSHOT_ERR_DEVICE;
+  }
+  g_scratch_ptr[device] = ptr;
+  return KVSHOT_OK;
+}
+
+void* scratch_ptr(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch_ptr[device];
+}
+
+// Bytes of split partials a plan writes: O [batch][Hkv][rows_pad][splits][D] float32, then
+// (m, l) [batch][Hkv][rows_pad][splits] float2 at the next 256-byte boundary.
+size_t partial_bytes(const kvshot_ctx* c, const Plan& pl, int batch, size_t* ml_offset) {
+  if (pl.splits <= 1) {
+    *ml_offset = 0;
+    return 0;
+  }
+  const size_t rows = (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * pl.splits;
+  *ml_offset = (rows * kHeadDim * sizeof(float) + 255) & ~(size_t)255;
+  return *ml_offset + rows * sizeof(float2);
+}
+
 void free_ctx(kvshot_ctx* c) {
   if (!c) return;
   const DeviceGuard dg(c->device);
@@ -343,6 +402,7 @@ const char* kvshot_status_string(int32_t s) {
     case KVSHOT_ERR_OUT_OF_MEMORY: return "device out of memory";
     case KVSHOT_ERR_DEVICE: return "HIP device error";
     case KVSHOT_ERR_DATA: return "contract violation in device data";
+    case KVSHOT_ERR_SCRATCH: return "the call's split partials exceed the no-allocation scratch buffer";
     default: return "unknown status";
   }
 }
@@ -415,6 +475,12 @@ kvshot_status kvshot_draft_attn_init(const kvshot_config* cfg, kvshot_handle* ou
     free_ctx(c);
     return KVSHOT_ERR_DEVICE;
   }
+  // the no-allocation call's scratch address on this device (resolved once per device)
+  const kvshot_status sst = resolve_scratch(c->device);
+  if (sst != KVSHOT_OK) {
+    free_ctx(c);
+    return sst;
+  }
   *out = c;
   return KVSHOT_OK;
 }
@@ -470,6 +536,26 @@ kvshot_status kvshot_draft_attn_tree(kvshot_handle h, int32_t batch, int32_t n_n
   a.lse = lse;
   return run_call(h, a, stream);
 }
+
+kvshot_status kvshot_draft_attn_call_noalloc(kvshot_handle h, const kvshot_call* call, void* stream) {
+  if (!h || !call) return KVSHOT_ERR_INVALID_ARG;
+  const kvshot_call& a = *call;
+  if (a.batch < 1 || a.batch > h->cfg.max_batch || a.n_queries < 1 || a.n_queries > h->cfg.max_draft ||
+      a.max_ctx_len_hint < 0)
+    return KVSHOT_ERR_INVALID_ARG;
+  void* base = scratch_ptr(h->device);
+  if (!base) return KVSHOT_ERR_DEVICE;
+  // the same plan as kvshot_draft_attn_call, so both return the same bits
+  const Plan pl = make_plan(h, a.batch, a.n_queries, a.max_ctx_len_hint);
+  size_t ml_off = 0;
+  if (partial_bytes(h, pl, a.batch, &ml_off) > kScratchBytes) return KVSHOT_ERR_SCRATCH;
+  Workspace ws;
+  ws.part_o = (float*)base;
+  ws.part_ml = (float2*)((unsigned char*)base + ml_off);
+  ws.profile = false;
+  return run_call(h, a, stream, &ws);
+}
+
 
 kvshot_status kvshot_draft_attn_call(kvshot_handle h, const kvshot_call* call, void* stream) {
   if (!call) return KVSHOT_ERR_INVALID_ARG;
