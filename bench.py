@@ -212,8 +212,9 @@ def main():
     ap.add_argument("--calls", type=int, default=None,
                     help="per-call timing sample for the median and p10/p90 (default: 100 for the 64 x 32K "
                          "workload, 200 otherwise; 0 skips it)")
-    ap.add_argument("--path", choices=["auto", "mfma", "generic"], default="auto",
-                    help="attention kernel: the planner's choice (bf16: MFMA), or forced")
+    ap.add_argument("--path", choices=["auto", "mfma", "generic", "general-mfma"], default="auto",
+                    help="attention kernel: the planner's choice (bf16: MFMA, 256-row tiles on the tall-tile "
+                         "kernel), or forced; general-mfma: the general MFMA kernel for every tile height")
     ap.add_argument("--cold", action="store_true",
                     help="flush the device caches (write 1 GiB) before every timed call; per-call events")
     ap.add_argument("--no-graph", action="store_true",
@@ -267,7 +268,7 @@ def main():
     if args.splits:
         att.set_option(K.OPT_SPLITS, args.splits)
     if args.path != "auto":
-        att.set_option(K.OPT_PATH, {"mfma": 1, "generic": 2}[args.path])
+        att.set_option(K.OPT_PATH, {"mfma": 1, "generic": 2, "general-mfma": 3}[args.path])
     nq_call = n if args.mode == "folded" else 1
     plan = att.plan(B, nq_call, T_max)
     edt = torch.bfloat16 if d["dtype"] == "bf16" else torch.float32

@@ -213,7 +213,9 @@ kvshot_status kvshot_draft_attn_validate(kvshot_handle h, int32_t batch, int32_t
 /* Tuning and introspection. */
 typedef enum {
   KVSHOT_OPT_SPLITS = 0,   /* value 0: automatic split-K count; n > 0: use n (clamped to the workspace) */
-  KVSHOT_OPT_PATH = 1,     /* 0 automatic, 1 MFMA kernel (bf16 only), 2 generic VALU kernel */
+  KVSHOT_OPT_PATH = 1,     /* 0 automatic, 1 MFMA kernels (bf16 only; 256-row query tiles take the
+                              tall-tile kernel), 2 generic VALU kernel, 3 the general MFMA kernel for
+                              every tile height (bf16 only) */
   KVSHOT_OPT_PROFILE = 2   /* 1: record HIP events around the attention and combine kernels of every call */
 } kvshot_option;
 kvshot_status kvshot_draft_attn_set_option(kvshot_handle h, int32_t option, int64_t value);

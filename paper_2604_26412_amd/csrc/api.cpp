@@ -95,10 +95,10 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_t
     pl.row_groups = 1;
     pl.waves_per_wg = 4;
     pl.key_streams = 1;
-  } else if (pl.row_tiles >= kTallRowTiles && allow_tall && use_tall_kernel()) {
+  } else if (pl.row_tiles >= kTallRowTiles && allow_tall && c->opt_path != 3 && use_tall_kernel()) {
     // 256-row tiles (draft trees, 33..64 queries at G = 4): the tall-tile kernel
     pl.path = 3;
-    pl.kernel_row_tiles = tall_waves_per_wg();
+    pl.kernel_row_tiles = kTallRowTiles;
     pl.row_groups = pl.row_tiles / pl.kernel_row_tiles;
     pl.waves_per_wg = tall_waves_per_wg();
     pl.key_streams = 1;
@@ -119,7 +119,7 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_t
     // blocks per wave.  (Each workgroup starts with a dependent chain of
     // loads -- length, page ids, K/V, RoPE table -- that only other resident
     // workgroups can hide, so more, shorter workgroups lose.)
-    const int per_cu = generic ? 2 : (pl.path == 3 ? 8 / pl.waves_per_wg : mfma_wgs_per_cu(pl.kernel_row_tiles));
+    const int per_cu = generic ? 2 : (pl.path == 3 ? 1 : mfma_wgs_per_cu(pl.kernel_row_tiles));
     const int target_wgs = c->num_cus * per_cu;
     splits = (target_wgs + pairs - 1) / pairs;
     const int cap = nb / (pl.key_streams * 4);
@@ -219,7 +219,7 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const 
   if (!aligned16(a.q) || !aligned16(a.k_pages) || !aligned16(a.v_pages) || !aligned16(a.draft_k) ||
       !aligned16(a.draft_v) || !aligned16(a.out))
     return KVSHOT_ERR_INVALID_ARG;
-  if (c->opt_path == 1 && g.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
+  if ((c->opt_path == 1 || c->opt_path == 3) && g.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
   const DeviceGuard dg(c->device);
   if (!dg.ok()) return KVSHOT_ERR_DEVICE;
   kvshot_status st = KVSHOT_OK;
@@ -594,8 +594,8 @@ kvshot_status kvshot_draft_attn_set_option(kvshot_handle h, int32_t option, int6
       h->opt_splits = (int)value;
       return KVSHOT_OK;
     case KVSHOT_OPT_PATH:
-      if (value < 0 || value > 2) return KVSHOT_ERR_INVALID_ARG;
-      if (value == 1 && h->cfg.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
+      if (value < 0 || value > 3) return KVSHOT_ERR_INVALID_ARG;
+      if ((value == 1 || value == 3) && h->cfg.dtype != KVSHOT_BF16) return KVSHOT_ERR_UNSUPPORTED;
       h->opt_path = (int)value;
       return KVSHOT_OK;
     case KVSHOT_OPT_PROFILE:

@@ -224,6 +224,27 @@ def test_tree_b8_ctx16k_n60_outlier_keys(outliers):
     _check_case(c, what=f"tree b8 ctx16k n60 outliers {no}x{sc:g}")
 
 
+@pytest.mark.parametrize("splits", [None, 1, 3])
+def test_tall_tiles_on_the_general_kernel(splits):
+    """256-row query tiles on the general MFMA kernel (path option 3; it also serves splits the
+    tall-tile kernel cannot stage, more than 512 blocks), with outlier keys; same bars.  The tall-tile
+    kernel raises a forced split count to its 512-block cap instead."""
+    parents = np.stack([W.random_tree(181, b, 60) for b in range(2)])
+    c = W.make_case(mode="tree", batch=2, ctx_lens=[17000, 3001], n_new=60, parents=parents, n_outlier=4,
+                    seed=181)
+    with G.handle_for(c) as att:
+        att.set_option(1, 3)
+        if splits:
+            att.set_option(0, splits)
+        plan = att.plan(2, 60, 17000)
+        assert plan["path"] == 1, plan
+        att.set_option(1, 1)
+        assert att.plan(2, 60, 17000)["path"] == 3
+        if splits == 1:
+            assert att.plan(2, 60, 17000)["splits"] == 2      # 532 blocks: raised to the cap
+    _check_case(c, splits=splits, path=3, what=f"tree on the general kernel, splits {splits}")
+
+
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
