@@ -183,8 +183,9 @@ kvshot_status kvshot_draft_attn_call(kvshot_handle h, const kvshot_call* call, v
  * allocates nothing and records no profiling events.
  *   - A call whose partials exceed 32 MiB (batch x num_kv_heads x padded rows
  *     x splits x (128 x 4 + 8) bytes, the partial (m, l) rows aligned to 256
- *     bytes; a one-split plan needs none) returns KVSHOT_ERR_SCRATCH and
- *     queues nothing.
+ *     bytes, plus 256 bytes of per-sequence split counts for a ragged batch;
+ *     a one-split plan needs none) returns KVSHOT_ERR_SCRATCH and queues
+ *     nothing.
  *   - Every call on one GPU shares that GPU's scratch: calls that overlap in
  *     time on one GPU (from any handle, stream or thread) race and give
  *     undefined results.  Calls ordered on one stream are safe.

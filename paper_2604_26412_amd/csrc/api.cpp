@@ -42,6 +42,7 @@ struct kvshot_ctx {
   float* part_o = nullptr;
   float2* part_ml = nullptr;
   int32_t* flag = nullptr;
+  int32_t* seq_splits = nullptr;   // [64]: per-sequence split counts of a balanced call
   size_t ws_rows = 0;       // capacity of the partial workspace in (row, split) entries
   int opt_splits = 0, opt_path = 0, opt_profile = 0;
   std::vector<ProfileSlot> prof;
@@ -65,6 +66,9 @@ struct Plan {
   int blocks_per_split;
   int rows, rows_pad;
   int waves_per_wg;
+  int balanced;    // length-balanced schedule: `items` work items per (KV head, row group)
+  int items;
+  int min_chunk;
 };
 
 // 32-row tiles from which the tall-tile kernel serves a call
@@ -140,6 +144,22 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_t
   if (pl.path == 3 && bps > tall_max_blocks()) return make_plan(c, batch, nq, max_ctx, false);
   pl.splits = splits;
   pl.blocks_per_split = bps;
+  // Ragged batches on the general MFMA kernel: share one round of work items per KV head out over
+  // the sequences in proportion to their lengths (computed on the device from ctx_lens), instead
+  // of giving every sequence the same split count.  Only when the items outnumber the sequences.
+  if (pl.path == 1 && c->opt_splits == 0 && batch >= 2 && batch <= 64) {
+    const int per_cu = mfma_wgs_per_cu(pl.kernel_row_tiles);
+    int items = c->num_cus * per_cu / (c->cfg.num_kv_heads * pl.row_groups);
+    if (items > c->max_splits) items = c->max_splits;
+    while (items > 1 && (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * items > c->ws_rows) --items;
+    if (items > batch) {
+      pl.balanced = 1;
+      pl.items = items;
+      pl.min_chunk = pl.key_streams * 2;
+      pl.splits = items;              // a sequence has at most `items` splits: the partials' stride
+      pl.blocks_per_split = 0;
+    }
+  }
   return pl;
 }
 
@@ -166,6 +186,9 @@ void fill_params(const kvshot_ctx* c, const Plan& pl, int batch, int nq, int max
   p.row_groups = pl.row_groups;
   p.splits = pl.splits;
   p.blocks_per_split = pl.blocks_per_split;
+  p.balanced = pl.balanced;
+  p.items = pl.items;
+  p.min_chunk = pl.min_chunk;
   p.max_ctx = max_ctx;
   p.max_position = (int32_t)g.max_position;
   p.out_fp32 = g.out_dtype == KVSHOT_FP32;
@@ -194,6 +217,7 @@ kvshot_status drain_profile(kvshot_ctx* c, bool all) {
 struct Workspace {
   float* part_o;
   float2* part_ml;
+  int32_t* seq_splits;
   bool profile;
 };
 
@@ -227,9 +251,11 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const 
   const Plan pl = make_plan(c, batch, nq, max_ctx);
   AttnParams p;
   fill_params(c, pl, batch, nq, max_ctx, p);
+  p.seq_splits = c->seq_splits;
   if (ws) {
     p.part_o = ws->part_o;
     p.part_ml = ws->part_ml;
+    p.seq_splits = ws->seq_splits;
   }
   p.q = a.q;
   p.k_pages = a.k_pages;
@@ -272,7 +298,7 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const 
   if (e != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (slot && hipEventRecord(slot->ev[1], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (pl.splits > 1) {
-    CombineParams cp;
+    CombineParams cp{};
     cp.part_o = p.part_o;
     cp.part_ml = p.part_ml;
     cp.out = out;
@@ -286,6 +312,7 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const 
     cp.rows_pad = pl.rows_pad;
     cp.splits = pl.splits;
     cp.out_fp32 = g.out_dtype == KVSHOT_FP32;
+    cp.seq_splits = pl.balanced ? p.seq_splits : nullptr;
     if (launch_combine(cp, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   }
   if (slot) {
@@ -364,16 +391,17 @@ void* scratch_ptr(int device) {
   return g_scratch_ptr[device];
 }
 
-// Bytes of split partials a plan writes: O [batch][Hkv][rows_pad][splits][D] float32, then
-// (m, l) [batch][Hkv][rows_pad][splits] float2 at the next 256-byte boundary.
-size_t partial_bytes(const kvshot_ctx* c, const Plan& pl, int batch, size_t* ml_offset) {
-  if (pl.splits <= 1) {
-    *ml_offset = 0;
-    return 0;
-  }
+// Scratch bytes a plan uses: split partials O [batch][Hkv][rows_pad][splits][D] float32, then
+// (m, l) [batch][Hkv][rows_pad][splits] float2, then the 64 per-sequence split counts of a
+// balanced plan, each at the next 256-byte boundary.
+size_t partial_bytes(const kvshot_ctx* c, const Plan& pl, int batch, size_t* ml_offset, size_t* seq_offset) {
+  *ml_offset = 0;
+  *seq_offset = 0;
+  if (pl.splits <= 1) return 0;
   const size_t rows = (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * pl.splits;
   *ml_offset = (rows * kHeadDim * sizeof(float) + 255) & ~(size_t)255;
-  return *ml_offset + rows * sizeof(float2);
+  *seq_offset = (*ml_offset + rows * sizeof(float2) + 255) & ~(size_t)255;
+  return *seq_offset + (pl.balanced ? 64 * sizeof(int32_t) : 0);
 }
 
 void free_ctx(kvshot_ctx* c) {
@@ -384,6 +412,7 @@ void free_ctx(kvshot_ctx* c) {
   if (c->part_o) (void)hipFree(c->part_o);
   if (c->part_ml) (void)hipFree(c->part_ml);
   if (c->flag) (void)hipFree(c->flag);
+  if (c->seq_splits) (void)hipFree(c->seq_splits);
   for (auto& s : c->prof)
     for (auto& e : s.ev)
       if (e) (void)hipEventDestroy(e);
@@ -466,7 +495,8 @@ kvshot_status kvshot_draft_attn_init(const kvshot_config* cfg, kvshot_handle* ou
   if (hipMalloc((void**)&c->rope, nrope * sizeof(float2)) != hipSuccess ||
       hipMalloc((void**)&c->part_o, c->ws_rows * kHeadDim * sizeof(float)) != hipSuccess ||
       hipMalloc((void**)&c->part_ml, c->ws_rows * sizeof(float2)) != hipSuccess ||
-      hipMalloc((void**)&c->flag, sizeof(int32_t)) != hipSuccess) {
+      hipMalloc((void**)&c->flag, sizeof(int32_t)) != hipSuccess ||
+      hipMalloc((void**)&c->seq_splits, 64 * sizeof(int32_t)) != hipSuccess) {
     (void)hipGetLastError();
     free_ctx(c);
     return KVSHOT_ERR_OUT_OF_MEMORY;
@@ -547,11 +577,12 @@ kvshot_status kvshot_draft_attn_call_noalloc(kvshot_handle h, const kvshot_call*
   if (!base) return KVSHOT_ERR_DEVICE;
   // the same plan as kvshot_draft_attn_call, so both return the same bits
   const Plan pl = make_plan(h, a.batch, a.n_queries, a.max_ctx_len_hint);
-  size_t ml_off = 0;
-  if (partial_bytes(h, pl, a.batch, &ml_off) > kScratchBytes) return KVSHOT_ERR_SCRATCH;
+  size_t ml_off = 0, seq_off = 0;
+  if (partial_bytes(h, pl, a.batch, &ml_off, &seq_off) > kScratchBytes) return KVSHOT_ERR_SCRATCH;
   Workspace ws;
   ws.part_o = (float*)base;
   ws.part_ml = (float2*)((unsigned char*)base + ml_off);
+  ws.seq_splits = (int32_t*)((unsigned char*)base + seq_off);
   ws.profile = false;
   return run_call(h, a, stream, &ws);
 }
@@ -628,7 +659,9 @@ kvshot_status kvshot_draft_attn_plan(kvshot_handle h, int32_t batch, int32_t n_q
   if (splits) *splits = pl.splits;
   if (path) *path = pl.path;
   if (row_tiles) *row_tiles = pl.row_tiles;
-  if (workgroups) *workgroups = pl.splits * pl.row_groups * h->cfg.num_kv_heads * batch;
+  if (workgroups)
+    *workgroups = pl.balanced ? pl.items * pl.row_groups * h->cfg.num_kv_heads
+                              : pl.splits * pl.row_groups * h->cfg.num_kv_heads * batch;
   return KVSHOT_OK;
 }
 

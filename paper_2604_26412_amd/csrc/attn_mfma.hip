@@ -87,21 +87,24 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   const int ks = w / RW;
   const int l32 = lane & 31;
   const int hh = lane >> 5;
-  int wi = xcd_remap(blockIdx.x, gridDim.x);       // work item: (row group, split, KV head, sequence)
+  int wi = xcd_remap(blockIdx.x, gridDim.x);
   const int rg = wi % p.row_groups;
   wi /= p.row_groups;
-  const int split = wi % p.splits;
-  wi /= p.splits;
-  const int h = wi % p.hkv;
-  const int b = wi / p.hkv;
+  int h, item = 0;
+  if (!p.balanced) {
+    wi /= p.splits;                                // (split, KV head, sequence); the split is decoded below
+    h = wi % p.hkv;
+  } else {
+    item = wi % p.items;                           // (item, KV head)
+    h = (wi / p.items) % p.hkv;
+  }
 
-  int T = clamp_ctx(p.ctx_lens[b], p.max_pages_per_seq, p.page_shift);
-  T = T > p.max_ctx ? p.max_ctx : T;
-  const int nbt = (T + kBlockKeys - 1) / kBlockKeys;
-  const int blk0 = split * p.blocks_per_split;
-  const int blk1 = min(blk0 + p.blocks_per_split, nbt);
+  // One split: query rows of sequence b (prefix length T) against its target blocks [blk0, blk1),
+  // plus its draft keys when `last`; written as part `part` of `nparts`, or as the output when
+  // nparts == 1.
+  auto segment = [&](const int b, const int T, const int part, const int nparts, const int blk0, const int blk1,
+                     const bool last) {
   const int nt = blk1 > blk0 ? blk1 - blk0 : 0;
-  const bool last = split == p.splits - 1;
 
   int s0 = 0, S = p.tree ? p.n_nodes : p.nq;
   if (!p.tree) {
@@ -543,11 +546,11 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   }
   if (ks != 0) return;
 
-  // ---- write: final output (one split) or split partial ----
+  // ---- write: final output (one part) or partial ----
 #pragma unroll
   for (int i = 0; i < TPW; ++i) {
     if (!row_ok[i]) continue;
-    if (p.splits == 1) {
+    if (nparts == 1) {
       const float inv = 1.0f / l_row[i];
       const int64_t orow = (((int64_t)b * p.nq + jrow[i]) * p.hq + hqr[i]) * kHeadDim;
 #pragma unroll
@@ -567,7 +570,7 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
       if (p.lse && hh == 0)
         p.lse[((int64_t)b * p.nq + jrow[i]) * p.hq + hqr[i]] = (M[i] + __log2f(l_row[i])) * kLn2;
     } else {
-      const int64_t prow = (((int64_t)b * p.hkv + h) * p.rows_pad + r[i]) * p.splits + split;
+      const int64_t prow = (((int64_t)b * p.hkv + h) * p.rows_pad + r[i]) * p.splits + part;
       float* po = p.part_o + prow * kHeadDim;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
@@ -580,6 +583,34 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
       if (hh == 0) p.part_ml[prow] = make_float2(M[i], l_row[i]);
     }
   }
+  };  // segment
+
+  if (!p.balanced) {
+    // every sequence split alike: work item (row group, split, KV head, sequence)
+    int wj = xcd_remap(blockIdx.x, gridDim.x) / p.row_groups;
+    const int split = wj % p.splits;
+    const int b = wj / p.splits / p.hkv;
+    int T = clamp_ctx(p.ctx_lens[b], p.max_pages_per_seq, p.page_shift);
+    T = T > p.max_ctx ? p.max_ctx : T;
+    const int nbt = (T + kBlockKeys - 1) / kBlockKeys;
+    const int blk0 = split * p.blocks_per_split;
+    segment(b, T, split, p.splits, blk0, min(blk0 + p.blocks_per_split, nbt), split == p.splits - 1);
+    return;
+  }
+  // length-balanced: this item's sequence and split, from the lengths
+  const BalancedSlot sl = balanced_schedule(p.ctx_lens, p.batch, p.max_ctx, p.max_pages_per_seq, p.page_shift,
+                                            p.items, p.min_chunk, lane);
+  const uint64_t own = __ballot(lane < p.batch && item >= sl.first && item < sl.first + sl.splits);
+  if (own == 0) return;                            // past the last split of the batch (whole workgroup)
+  const int b = __builtin_amdgcn_readfirstlane(__builtin_ctzll(own));
+  const int nsplit = __builtin_amdgcn_readfirstlane(__shfl(sl.splits, b));
+  const int split = item - __builtin_amdgcn_readfirstlane(__shfl(sl.first, b));
+  const int per = __builtin_amdgcn_readfirstlane(__shfl(sl.per, b));
+  const int T = __builtin_amdgcn_readfirstlane(__shfl(sl.ctx, b));
+  // the combine reads each sequence's split count (one writer per sequence)
+  if (split == 0 && h == 0 && rg == 0 && threadIdx.x == 0) p.seq_splits[b] = nsplit;
+  const int nbt = (T + kBlockKeys - 1) / kBlockKeys;
+  segment(b, T, split, nsplit, split * per, min(split * per + per, nbt), split == nsplit - 1);
 }
 
 }  // namespace
@@ -645,7 +676,8 @@ int mfma_kernel_row_tiles(int row_tiles) {
 }
 
 hipError_t launch_attn_mfma(const AttnParams& p, int kernel_row_tiles, hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)p.splits * p.row_groups * p.hkv * p.batch));
+  const dim3 grid((unsigned)(p.balanced ? (int64_t)p.items * p.row_groups * p.hkv
+                                         : (int64_t)p.splits * p.row_groups * p.hkv * p.batch));
   constexpr bool q1 = KVSHOT_QSPLIT_MAX_RT >= 1, q2 = KVSHOT_QSPLIT_MAX_RT >= 2, q4 = KVSHOT_QSPLIT_MAX_RT >= 4,
                  q8 = KVSHOT_QSPLIT_MAX_RT >= 8;
   switch (kernel_row_tiles) {

@@ -73,7 +73,15 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int j = r / p.group;
   const int hq = h * p.group + (r - j * p.group);
   const int64_t q_index = ((int64_t)b * p.nq + j) * p.hq + hq;
-  combine_row(p.part_o, p.part_ml, (bh * p.rows_pad + r) * p.splits, p.splits, p.out, q_index * kHeadDim,
+  int splits = p.splits;
+  if (p.seq_splits) {
+    // this sequence's split count under the attention kernel's balanced schedule; with one split the
+    // attention kernel wrote the output itself
+    splits = p.seq_splits[b];
+    if (splits <= 1) return;
+    splits = splits > p.splits ? p.splits : splits;
+  }
+  combine_row(p.part_o, p.part_ml, (bh * p.rows_pad + r) * p.splits, splits, p.out, q_index * kHeadDim,
               p.out_fp32 != 0, p.lse ? p.lse + q_index : nullptr, lane);
 }
 

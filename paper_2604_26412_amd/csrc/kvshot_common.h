@@ -46,6 +46,13 @@ struct AttnParams {
   int32_t n_nodes;              // tree mode: draft-tree nodes (draft keys) per sequence
   int32_t out_fp32;
   float qscale;                 // softmax scale * log2(e): scores come out in log2 units
+  // Length-balanced schedule (batch <= 64): `items` work items per (KV head, row group) are shared
+  // out over the sequences in proportion to their lengths (balanced_schedule); `splits` is then
+  // the stride of a sequence's partials, an upper bound of its split count.
+  int32_t balanced;
+  int32_t items;
+  int32_t min_chunk;            // blocks per item at least (a multiple of the key streams)
+  int32_t* seq_splits;          // [batch]: each sequence's split count, written for the combine
 };
 
 struct CombineParams {
@@ -54,6 +61,8 @@ struct CombineParams {
   void* out;
   float* lse;
   int32_t batch, nq, hq, hkv, group, rows, rows_pad, splits, out_fp32;
+  // balanced schedule: each sequence's split count, written by the attention kernel (null: `splits`)
+  const int32_t* seq_splits;
 };
 
 // ---------------------------------------------------------------------------
@@ -120,6 +129,60 @@ __device__ __forceinline__ int query_node(const AttnParams& p, int b, int j) {
   if (!p.query_nodes) return j;
   const int v = p.query_nodes[(int64_t)b * p.nq + j];
   return v < 0 ? 0 : (v >= p.n_nodes ? p.n_nodes - 1 : v);
+}
+
+// Length-balanced split schedule, evaluated by one wave (batch <= 64, lane b = sequence b).
+// Sequence b has nb_b = ceil(T_b / 32) prefix blocks (T_b clamped as the kernels clamp it).  The
+// chunk is the smallest multiple of min_chunk whose split counts splits_b = max(1, ceil(nb_b /
+// chunk)) sum to at most `items` (or the longest prefix, when even one split each does not fit).
+// Sequence b owns work items [first_b, first_b + splits_b); its prefix is cut evenly, split s
+// covering blocks [s per_b, (s + 1) per_b) with per_b = ceil(nb_b / splits_b) <= chunk, so the
+// last split is never empty.  A pure function of the lengths.
+struct BalancedSlot {
+  int ctx;      // this lane's sequence: prefix length (clamped)
+  int splits;   // its split count
+  int per;      // its blocks per split
+  int first;    // exclusive prefix of split counts
+};
+__device__ __forceinline__ BalancedSlot balanced_schedule(const int32_t* ctx_lens, int batch, int max_ctx,
+                                                          int max_pages_per_seq, int page_shift, int items,
+                                                          int min_chunk, int lane) {
+  int nb = 0, t = 0;
+  if (lane < batch) {
+    t = clamp_ctx(ctx_lens[lane], max_pages_per_seq, page_shift);
+    t = t > max_ctx ? max_ctx : t;
+    nb = (t + kBlockKeys - 1) / kBlockKeys;
+  }
+  int maxnb = nb;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) maxnb = max(maxnb, __shfl_xor(maxnb, o));
+  auto total_splits = [&](int chunk) {
+    int v = lane < batch ? max(1, (nb + chunk - 1) / chunk) : 0;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+  };
+  // chunk = min_chunk * k: the smallest k in [1, kmax] that fits (kmax covers the longest prefix)
+  const int kmax = max(1, (maxnb + min_chunk - 1) / min_chunk);
+  int lo = 1, hi = kmax;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (total_splits(mid * min_chunk) <= items) hi = mid;
+    else lo = mid + 1;
+  }
+  const int chunk = lo * min_chunk;
+  BalancedSlot r;
+  r.ctx = t;
+  r.splits = lane < batch ? max(1, (nb + chunk - 1) / chunk) : 0;
+  r.per = lane < batch ? (nb + r.splits - 1) / r.splits : 0;
+  int incl = r.splits;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  r.first = incl - r.splits;
+  return r;
 }
 
 // Element offset of draft row s of sequence b, KV head h.
