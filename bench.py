@@ -205,6 +205,8 @@ def main():
                              "fusion_t64_d4096", "fusion_t480_d4096", "kvproj_prefill_b64_t32k",
                              "kvproj_verify_b64_t32k", "accept_n64m_k7", "treegrow_b8_v152k_d8k10n60"])
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
+    ap.add_argument("--kvproj-path", type=int, default=0, choices=[0, 1, 2],
+                    help="--op kvproj: 0 automatic, 1 the tiled kernel, 2 the direct kernel")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--contiguous", action="store_true",
@@ -623,8 +625,8 @@ def kvproj_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_kvproj_traffic(workload: str):
-    path = os.path.join(PROFILES, f"kvproj_kernel_{workload}_counters.md")
+def read_kvproj_traffic(workload: str, kernel: str = "kvproj_kernel"):
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -753,6 +755,8 @@ def bench_kvproj(args, torch, K, W):
                           num_pages=d["pool"], max_tokens=n, max_position=d["pps"] * P)
     if args.splits:
         proj.set_option(K.OPT_SPLITS, args.splits)
+    if args.kvproj_path:
+        proj.set_option(K.OPT_PATH, args.kvproj_path)
     plan = proj.plan(n)
 
     def step():
@@ -814,8 +818,13 @@ def bench_kvproj(args, torch, K, W):
     else:
         roof = {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = read_kvproj_traffic(name) if not (args.splits or args.no_rope) else None
-    roof.update({"kernel": f"kvproj_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)",
+    kfile = "kvproj_direct_kernel" if plan["path"] == 2 else "kvproj_kernel"
+    roof["traffic"] = read_kvproj_traffic(name, kfile) if not (args.splits or args.no_rope or args.kvproj_path) else None
+    if plan["path"] == 2:
+        kname = f"kvproj_direct_kernel ({plan['tile_tokens']}-token tiles, {plan['workgroups']} workgroups)"
+    else:
+        kname = f"kvproj_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)"
+    roof.update({"kernel": kname,
                  "kernel_ms": round(main_ms, 5), "combine_ms": round(comb_ms, 5),
                  "algorithmic_bytes_per_launch": main_bytes, "flops_per_launch": alg["flops"],
                  "arithmetic_intensity_flop_per_byte": round(intensity, 1),
@@ -835,7 +844,8 @@ def bench_kvproj(args, torch, K, W):
         "data": "synthetic",
         "config": {"workload": f"{name}: {d['B']} sequences x {d['T']} tokens cached, {n} tokens projected, "
                                f"L_s {L}, d_kv {d_kv}, pages of {P}, random page table, bf16",
-                   "tokens": n, "layers": L, "d_kv": d_kv, "rope": rope, "splits": plan["splits"],
+                   "tokens": n, "layers": L, "d_kv": d_kv, "rope": rope, "path": plan["path"],
+                   "tile_tokens": plan["tile_tokens"], "splits": plan["splits"],
                    "workgroups": plan["workgroups"], "launch": "python" if args.no_graph else "hip graph replay"},
         "roofline": roof,
         "step_tflops": round(alg["flops"] / (ms_per_step * 1e-3) / 1e12, 2),

@@ -22,8 +22,10 @@
  * engine keeps them).
  *
  * Arithmetic: bf16 products on MFMA with float32 accumulation over the
- * L_s d_kv inputs (with split reductions, in a fixed order per plan);
- * RoPE in float32 from a table built in float64; one rounding to bf16.
+ * L_s d_kv inputs (in a fixed order per plan: split reductions on the tiled
+ * path, per-wave partial sums added in wave order on the direct path); RoPE
+ * in float32 (a table built in float64, or on the tiled path without splits
+ * angles reduced in float64); one rounding to bf16.
  *
  * Conventions (as in kvshot_draft_attn.h): array pointers are DEVICE pointers
  * unless marked (host); bf16 is passed as raw 16-bit patterns; the caller owns
@@ -110,13 +112,20 @@ kvshot_status kvshot_kv_project_validate(kvshot_kvproj_handle h, int32_t n_token
                                          int32_t* bad_token, int32_t* bad_code, void* stream);
 
 /* Options: KVSHOT_OPT_SPLITS (0 automatic, else 1 .. 16 workgroups along the
- * reduction, capped by the workspace) and KVSHOT_OPT_PROFILE (1: HIP events
- * around each kernel of every call), as for the attention handle. */
+ * reduction of the tiled path, capped by the workspace), KVSHOT_OPT_PATH
+ * (0 automatic: the direct path where the tiled one would split its
+ * reduction, unless KVSHOT_OPT_SPLITS is set; 1 the tiled path, 256 channels x
+ * 256 tokens per workgroup; 2 the direct path, 64 channels x up to 64 tokens
+ * per workgroup with the whole reduction, no partial sums) and
+ * KVSHOT_OPT_PROFILE (1: HIP events around each kernel of every call), as for
+ * the attention handle. */
 kvshot_status kvshot_kvproj_set_option(kvshot_kvproj_handle h, int32_t option, int64_t value);
 
-/* Plan of a call with n_tokens tokens: reduction splits and workgroups of the
- * main kernel.  Host outputs, each nullable. */
-kvshot_status kvshot_kvproj_plan(kvshot_kvproj_handle h, int32_t n_tokens, int32_t* splits, int32_t* workgroups);
+/* Plan of a call with n_tokens tokens: reduction splits (1 on the direct
+ * path), path (1 tiled, 2 direct), tokens per workgroup tile and workgroups of
+ * the main kernel.  Host outputs, each nullable. */
+kvshot_status kvshot_kvproj_plan(kvshot_kvproj_handle h, int32_t n_tokens, int32_t* splits, int32_t* path,
+                                 int32_t* tile_tokens, int32_t* workgroups);
 
 /* With KVSHOT_OPT_PROFILE on: synchronises, then returns the summed event time
  * (ms) of the main kernel and of the split combine kernel since the last read,

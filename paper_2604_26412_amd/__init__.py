@@ -132,7 +132,8 @@ def load_library(path: Optional[str] = None):
         "kvshot_kv_project_validate": [_vp, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_i32),
                                        ctypes.POINTER(_i32), _vp],
         "kvshot_kvproj_set_option": [_vp, _i32, _i64],
-        "kvshot_kvproj_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32)],
+        "kvshot_kvproj_plan": [_vp, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i32),
+                               ctypes.POINTER(_i32)],
         "kvshot_kvproj_profile_read": [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(_i64)],
         "kvshot_acceptance_stats": [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i32, _vp],
@@ -751,10 +752,10 @@ class KvProjection:
         _check("kvshot_kvproj_set_option", self._lib.kvshot_kvproj_set_option(self._h, option, value))
 
     def plan(self, n_tokens: int):
-        s, w = _i32(0), _i32(0)
-        _check("kvshot_kvproj_plan", self._lib.kvshot_kvproj_plan(self._h, n_tokens, ctypes.byref(s),
-                                                                  ctypes.byref(w)))
-        return dict(splits=s.value, workgroups=w.value)
+        s, p, t, w = _i32(0), _i32(0), _i32(0), _i32(0)
+        _check("kvshot_kvproj_plan", self._lib.kvshot_kvproj_plan(self._h, n_tokens, ctypes.byref(s), ctypes.byref(p),
+                                                                  ctypes.byref(t), ctypes.byref(w)))
+        return dict(splits=s.value, path=p.value, tile_tokens=t.value, workgroups=w.value)
 
     def profile_read(self):
         a, c, k = ctypes.c_double(0), ctypes.c_double(0), _i64(0)

@@ -35,6 +35,11 @@
 // hardware hands workgroup i to XCD i % 8; xcd_remap gives each XCD a
 // contiguous range, so the channel tiles that read one token tile share that
 // XCD's L2.
+//
+// Calls with few tokens (where this tiling would split the reduction) take
+// kvproj_direct_kernel instead: 64-channel x up-to-64-token tiles that keep
+// the whole reduction, so no float32 partials go to memory and no combine
+// kernel runs.
 #include <type_traits>
 
 #include "kvproj_common.h"
@@ -340,6 +345,229 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
   }
 }
 
+// ---- direct kernel: calls with few tokens ----
+// A workgroup owns one RoPE pair of 32-channel slices of a head (channels
+// 32 s .. 32 s + 31 and their partners + 64: tile rows 0..31 and 32..63) x
+// 16 TB tokens, and the whole reduction, so no partial sums leave the chip.
+// The reduction runs in chunks of 128 inputs (one head of one source layer:
+// 256 contiguous bytes of every weight row and of every token's page slot).
+// Each chunk goes into an NBUF-stage LDS ring with global_load_lds_dwordx4,
+// four rows of 256 bytes per wave-wide load, so that neighbouring lanes read
+// neighbouring bytes: loading the MFMA fragments straight from global memory
+// (each lane a different row) moves a third as many bytes per CU per second
+// from L2.  The four waves take one 32-wide k-step of every chunk each
+// (v_mfma_f32_16x16x32_bf16 over the whole 64 x 16 TB tile) and add their
+// sums through LDS at the end in wave order; keys are then rotated (angles
+// reduced in float64, hardware sine and cosine), rounded and stored.  The work
+// order puts a channel slice's token tiles next to each other, so they run on
+// one XCD and its weight rows come from HBM once.
+template <int TB, int NBUF>
+__global__ __launch_bounds__(256, 1) void kvproj_direct_kernel(KvProjParams p) {
+  constexpr int NW = 4;
+  constexpr int kTok = 16 * TB;
+  constexpr int kRowB = 256;                       // bytes of a row of a chunk
+  constexpr int kStage = (64 + kTok) * kRowB;      // weight rows, then token rows
+  constexpr int kLA = 64 / 4 / NW;                 // weight loads per wave and chunk (4 rows each)
+  constexpr int kLB = kTok / 4 / NW;               // token loads per wave and chunk
+  constexpr int kLoads = kLA + kLB;
+  constexpr int kRow = 68;                         // floats per token row of the merge buffer (64 + 4 of padding)
+  static_assert(NBUF >= 2 && NBUF * kStage <= 150 * 1024, "ring fits in LDS");
+  static_assert(NW * kTok * kRow * 4 <= NBUF * kStage, "merge buffer fits in the ring");
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) unsigned char ring[NBUF * kStage];
+  __shared__ int64_t t_src[kTok];
+  __shared__ int64_t t_dst[kTok];
+  __shared__ int32_t t_pos[kTok];
+  __shared__ double t_rev[kHalfDim];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wi = xcd_remap(blockIdx.x, gridDim.x);
+  if (wi >= p.work_items) return;
+  const int tt = wi % p.n_tiles;                  // token tile
+  const int ct = wi / p.n_tiles;                  // channel slice: tensor, head, half
+  const int pairs = 2 * p.hkv;
+  const int g = ct / pairs;                       // 0: keys, 1: values
+  const int head = (ct % pairs) >> 1;
+  const int half = ct & 1;
+  const int n0 = tt * kTok;
+  const int d_kv = p.hkv * kHeadDim;
+  const int K = p.layers * d_kv;
+  const int nch = K / kHeadDim;                   // chunks: (layer, head) of the sources
+
+  if (tid < kTok) {
+    const int tk = n0 + tid < p.n_tokens ? n0 + tid : p.n_tokens - 1;
+    const int b = clampi(p.token_seq[tk], 0, p.batch - 1);
+    const int t = clampi(p.token_pos[tk], 0, (p.max_pages_per_seq << p.page_shift) - 1);
+    const int lp = t >> p.page_shift;
+    const int slot = t & ((1 << p.page_shift) - 1);
+    const int sp = physical_page(p.page_table, b, p.max_pages_per_seq, lp, p.num_pages);
+    const int dp = physical_page(p.dst_page_table, b, p.max_pages_per_seq, lp, p.dst_num_pages);
+    t_src[tid] = (int64_t)sp * p.page_stride + (int64_t)slot * p.slot_stride;
+    t_dst[tid] = (int64_t)dp * p.dst_page_stride + (int64_t)slot * p.dst_slot_stride;
+    t_pos[tid] = t < p.max_position ? t : p.max_position - 1;
+  } else if (tid >= 128 && tid < 128 + kHalfDim) {
+    t_rev[tid - 128] = p.rope_rev[tid - 128];
+  }
+  __syncthreads();
+
+  // ---- loads: lane L of a wave-wide load fills row (4 rows per load) L / 16, physical 16-byte piece
+  // L % 16, holding logical piece (L % 16) ^ (row % 16) (so the fragment reads below are free of bank
+  // conflicts).  Wave w loads weight rows 16 w .. 16 w + 15 and token rows 4 TB w .. 4 TB w + 4 TB - 1. ----
+  const int lrow = lane >> 4;
+  const uint16_t* wsrc = g ? p.w_v : p.w_k;
+  int32_t aoff[kLA];     // element offsets in the weight matrix (chunk 0)
+  int64_t boff[kLB];     // element offsets in a source pool (chunk 0 of the token's slot)
+#pragma unroll
+  for (int i = 0; i < kLA; ++i) {
+    const int R = 16 * w + 4 * i + lrow;
+    const int ch = head * kHeadDim + 32 * half + (R & 31) + 64 * (R >> 5);
+    aoff[i] = ch * K + 8 * ((lane & 15) ^ (R & 15));
+  }
+#pragma unroll
+  for (int j = 0; j < kLB; ++j) {
+    const int R = 4 * kLB * w + 4 * j + lrow;
+    boff[j] = t_src[R] + 8 * ((lane & 15) ^ (R & 15));
+  }
+  const uint16_t* src_l0 = g ? p.v_src[0] : p.k_src[0];
+  const uint16_t* src_l1 = g ? p.v_src[1] : p.k_src[1];
+  const uint16_t* src_l2 = g ? p.v_src[2] : p.k_src[2];
+  const uint16_t* src_l3 = g ? p.v_src[3] : p.k_src[3];
+  // the kLoads loads of chunk c into `stage`: weight rows first, then token rows
+  struct Target {
+    const uint16_t* wc;    // the chunk's columns of the weight rows
+    const uint16_t* x;     // the chunk's (layer, head) in the source pool
+    unsigned char* st;     // the stage
+  };
+  auto target = [&](int c, int stage) {
+    const int l = c / p.hkv;
+    const int hd = c - l * p.hkv;
+    const uint16_t* x = l == 0 ? src_l0 : (l == 1 ? src_l1 : (l == 2 ? src_l2 : src_l3));
+    Target t;
+    t.x = x + (int64_t)hd * p.head_stride;
+    t.wc = wsrc + c * kHeadDim;
+    t.st = ring + stage * kStage;
+    return t;
+  };
+  auto issue_one = [&](const Target& t, int idx) {
+    if (idx < kLA) load_to_lds16(t.wc + aoff[idx], t.st + (16 * w + 4 * idx) * kRowB);
+    else load_to_lds16(t.x + boff[idx - kLA], t.st + (64 + 4 * kLB * w + 4 * (idx - kLA)) * kRowB);
+  };
+
+  // ---- fragments: wave w takes k-step w of every chunk (inputs 32 w .. 32 w + 31 of the head): lane
+  // (r = l % 16, q = l / 16) reads logical piece 4 w + q of rows 16 i + r (weights) and 64 + 16 j + r (tokens) ----
+  const int r = lane & 15, q = lane >> 4;
+  const int frag = r * kRowB + 16 * ((4 * w + q) ^ r);
+  f32x4 acc[4][TB];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // One chunk from `stage`, with the loads of a later chunk (`nt`, if `more`) spread between its MFMAs:
+  // a wave that waits to hand a load to the address unit then has matrix work in flight, instead of
+  // issuing a burst of loads and then computing.  The order is pinned with scheduling barriers.
+  auto compute = [&](int stage, const Target& nt, bool more) {
+    const unsigned char* st = ring + stage * kStage + frag;
+    bf16x8 a[4], bv[TB];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = as_bf16x8(*(const u32x4*)(st + 16 * i * kRowB));
+#pragma unroll
+    for (int j = 0; j < TB; ++j) bv[j] = as_bf16x8(*(const u32x4*)(st + (64 + 16 * j) * kRowB));
+#pragma unroll
+    for (int m = 0; m < 4 * TB; ++m) {
+      const int i = m / TB, j = m % TB;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
+      // load k goes after MFMA (k * 4 TB) / kLoads, so the kLoads loads spread evenly over the 4 TB MFMAs
+#pragma unroll
+      for (int k = 0; k < kLoads; ++k)
+        if ((k * 4 * TB) / kLoads == m) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (more) issue_one(nt, k);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+  };
+
+  // ---- ring: chunks 0 .. NBUF - 2 up front; iteration c waits for its own loads of chunk c (the younger
+  // chunks in flight may stay so), passes a barrier (all of chunk c has landed and every wave is done
+  // with chunk c - 1), issues chunk c + NBUF - 1 into the stage chunk c - 1 used, and computes c. ----
+#pragma unroll
+  for (int c = 0; c < NBUF - 1; ++c)
+    if (c < nch) {
+      const Target t = target(c, c);
+#pragma unroll
+      for (int k = 0; k < kLoads; ++k) issue_one(t, k);
+    }
+  int stage = 0;
+  for (int c = 0; c < nch; ++c) {
+    const int younger = nch - 1 - c;              // chunks issued after c (at most NBUF - 2)
+    if (younger >= NBUF - 2) wait_vmcnt<(NBUF - 2) * kLoads>();
+    else if (NBUF > 3 && younger == NBUF - 3) wait_vmcnt<(NBUF > 3 ? NBUF - 3 : 0) * kLoads>();
+    else if (NBUF > 4 && younger == NBUF - 4) wait_vmcnt<(NBUF > 4 ? NBUF - 4 : 0) * kLoads>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    const int nxt = c + NBUF - 1;
+    compute(stage, target(nxt < nch ? nxt : nch - 1, stage == 0 ? NBUF - 1 : stage - 1), nxt < nch);
+    stage = stage == NBUF - 1 ? 0 : stage + 1;
+  }
+
+  // ---- merge: wave w's sums at red[w][token][row] (the ring, free once every wave is past the last chunk);
+  // lane l of block (i, j) holds rows 16 i + 4 (l / 16) .. + 3 of token 16 j + l % 16 ----
+  lds_barrier();
+  float* red = (float*)ring;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j)
+      *(f32x4*)(red + (w * kTok + 16 * j + r) * kRow + 16 * i + 4 * q) = acc[i][j];
+  __syncthreads();
+
+  // item (token n, quad e4): channels 32 half + 4 e4 .. + 3 (tile rows 4 e4 ..) and their partners + 64
+  uint16_t* dst_base = (g ? p.v_dst : p.k_dst) + (int64_t)head * p.dst_head_stride + 32 * half;
+  const bool rot = g == 0 && p.rope_keys;
+  for (int item = tid; item < kTok * 8; item += NW * 64) {
+    const int n = item >> 3, e4 = item & 7;
+    if (n0 + n >= p.n_tokens) continue;
+    float x1[4] = {0.f, 0.f, 0.f, 0.f}, x2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) {
+      const float* row = red + (ww * kTok + n) * kRow;
+      const f32x4 u = *(const f32x4*)(row + 4 * e4);
+      const f32x4 v = *(const f32x4*)(row + 32 + 4 * e4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x1[e] += u[e];
+        x2[e] += v[e];
+      }
+    }
+    if (rot) {
+      // angle of channel pair m at position t: t theta^(-2m/128) = t rev[m] revolutions, reduced to
+      // [0, 1) in float64 before the hardware sine and cosine (input in revolutions)
+      const double pos = (double)t_pos[n];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        double rv = pos * t_rev[32 * half + 4 * e4 + e];
+        rv -= floor(rv);
+        const float u = (float)rv;
+        const float cs = __builtin_amdgcn_cosf(u), sn = __builtin_amdgcn_sinf(u);
+        const float y1 = x1[e] * cs - x2[e] * sn;
+        const float y2 = x2[e] * cs + x1[e] * sn;
+        x1[e] = y1;
+        x2[e] = y2;
+      }
+    }
+    uint16_t* dst = dst_base + t_dst[n] + 4 * e4;
+    u32x2 lo, hi;
+    lo[0] = pack_bf16x2(x1[0], x1[1]);
+    lo[1] = pack_bf16x2(x1[2], x1[3]);
+    hi[0] = pack_bf16x2(x2[0], x2[1]);
+    hi[1] = pack_bf16x2(x2[2], x2[3]);
+    *(u32x2*)dst = lo;
+    *(u32x2*)(dst + 64) = hi;
+  }
+}
+
 // Sum of the split partials, RoPE on keys, bf16 rounding, scatter.  Thread =
 // (token, tensor, head, quad q): channels 4q .. 4q + 3 and 64 + 4q .. + 3.
 __global__ __launch_bounds__(256) void kvproj_combine_kernel(KvProjParams p) {
@@ -423,6 +651,25 @@ hipError_t launch_kvproj(const KvProjParams& p, hipStream_t s) {
     hipLaunchKernelGGL((kvproj_kernel<true, KC, NS>), dim3(grid), dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL((kvproj_kernel<false, KC, NS>), dim3(grid), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+#ifndef KVSHOT_KVPROJ_DIRECT_NBUF
+#define KVSHOT_KVPROJ_DIRECT_NBUF 4
+#endif
+
+hipError_t launch_kvproj_direct(const KvProjParams& p, hipStream_t s) {
+  // ring stages: KVSHOT_KVPROJ_DIRECT_NBUF, fewer where (64 + 16 tile16) rows of 256 bytes per stage do not fit
+  constexpr int NB = KVSHOT_KVPROJ_DIRECT_NBUF;
+  constexpr int NB4 = NB * 32 * 1024 <= 150 * 1024 ? NB : 4;
+  const dim3 grid((p.work_items + 7) / 8 * 8), block(256);
+  switch (p.tile16) {
+    case 1: hipLaunchKernelGGL((kvproj_direct_kernel<1, NB>), grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL((kvproj_direct_kernel<2, NB>), grid, block, 0, s, p); break;
+    case 3: hipLaunchKernelGGL((kvproj_direct_kernel<3, NB>), grid, block, 0, s, p); break;
+    case 4: hipLaunchKernelGGL((kvproj_direct_kernel<4, NB4>), grid, block, 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

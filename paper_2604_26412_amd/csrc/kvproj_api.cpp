@@ -32,7 +32,7 @@ struct kvshot_kvproj_ctx {
   float* part = nullptr;
   size_t ws_rows = 0;           // capacity of the partial workspace in (split, token) rows of 2 d_kv floats
   int32_t* flag = nullptr;
-  int opt_splits = 0, opt_profile = 0;
+  int opt_splits = 0, opt_profile = 0, opt_path = 0;
   std::vector<ProjProfileSlot> prof;
   int64_t prof_head = 0, prof_tail = 0;
   double main_ms = 0.0, combine_ms = 0.0;
@@ -63,6 +63,66 @@ int plan_splits(const kvshot_kvproj_ctx* c, int n_tokens) {
   if (s > chunks_of(c)) s = chunks_of(c);
   while (s > 1 && (size_t)s * n_tokens > c->ws_rows) --s;
   return s < 1 ? 1 : s;
+}
+
+// Plan of a call.  Path 1 is the tiled kernel (256 channels x 256 tokens per
+// workgroup, split reductions when that grid is below one workgroup per CU);
+// path 2 the direct kernel (64 channels x 16 tile16 tokens per workgroup, the
+// whole reduction in one workgroup, no partial sums).  The direct tile height
+// minimises the operand bytes of the busiest CU: ceil(workgroups / CUs) x
+// (64 + 16 tile16) rows of the reduction.  The automatic choice compares two
+// estimates fitted to MI355X timings (Hkv 4 to 16, 64 to 16384 tokens): a
+// direct round costs about 4 us plus its operand rows at 60 GB/s per CU (one
+// workgroup per CU), a tiled round 6 us plus 512 rows at 32 GB/s per CU, and
+// split partials are written and read back at about 5 TB/s plus 2 us.
+struct ProjPlan {
+  int path = 1, splits = 1, tile16 = 0, tiles = 0, workgroups = 0;
+};
+
+ProjPlan direct_plan(const kvshot_kvproj_ctx* c, int n_tokens, double* est_us) {
+  ProjPlan pl;
+  pl.path = 2;
+  const int64_t slices = 4ll * c->cfg.num_kv_heads;   // (tensor, head, half)
+  const double row_bytes = 2.0 * c->cfg.num_layers * c->cfg.num_kv_heads * kHeadDim;
+  double best = -1.0;
+  for (int tb = 1; tb <= kProjDirectMaxTile16; ++tb) {
+    const int64_t tiles = (n_tokens + 16 * tb - 1) / (16 * tb);
+    const int64_t wgs = slices * tiles;
+    const int64_t rounds = (wgs + c->num_cus - 1) / c->num_cus;
+    const double us = (double)rounds * (4.0 + (64 + 16 * tb) * row_bytes / 60e3);
+    if (best < 0 || us < best) {
+      best = us;
+      pl.tile16 = tb;
+      pl.tiles = (int)tiles;
+      pl.workgroups = (int)wgs;
+    }
+  }
+  *est_us = best;
+  return pl;
+}
+
+ProjPlan tiled_plan(const kvshot_kvproj_ctx* c, int n_tokens, double* est_us) {
+  ProjPlan pl;
+  pl.path = 1;
+  pl.splits = plan_splits(c, n_tokens);
+  pl.tiles = n_tiles_of(n_tokens);
+  pl.workgroups = 2 * m_tiles_of(c) * pl.tiles * pl.splits;
+  const double row_bytes = 2.0 * c->cfg.num_layers * c->cfg.num_kv_heads * kHeadDim / pl.splits;
+  const int64_t rounds = (pl.workgroups + c->num_cus - 1) / c->num_cus;
+  double us = (double)rounds * (6.0 + 512 * row_bytes / 32e3);
+  if (pl.splits > 1)
+    us += 2.0 + 2.0 * pl.splits * (double)n_tokens * 2 * c->cfg.num_kv_heads * kHeadDim * 4 / 5e6;
+  *est_us = us;
+  return pl;
+}
+
+ProjPlan make_plan(const kvshot_kvproj_ctx* c, int n_tokens) {
+  double td = 0.0, tt = 0.0;
+  const ProjPlan d = direct_plan(c, n_tokens, &td);
+  const ProjPlan t = tiled_plan(c, n_tokens, &tt);
+  if (c->opt_path == 2) return d;
+  if (c->opt_path == 1 || c->opt_splits > 0) return t;
+  return td < tt ? d : t;
 }
 
 void free_proj(kvshot_kvproj_ctx* c) {
@@ -242,8 +302,11 @@ kvshot_status kvshot_kv_project(kvshot_kvproj_handle h, int32_t n_tokens, int32_
   p.k_dst = (uint16_t*)k_dst;
   p.v_dst = (uint16_t*)v_dst;
   p.rope_keys = (flags & KVSHOT_KVPROJ_ROPE) ? 1 : 0;
-  p.splits = plan_splits(h, n_tokens);
-  p.work_items = 2 * p.m_tiles * p.n_tiles * p.splits;
+  const ProjPlan pl = make_plan(h, n_tokens);
+  p.splits = pl.splits;
+  p.n_tiles = pl.tiles;
+  p.tile16 = pl.tile16;
+  p.work_items = pl.workgroups;
   hipStream_t s = (hipStream_t)stream;
 
   ProjProfileSlot* slot = nullptr;
@@ -255,7 +318,7 @@ kvshot_status kvshot_kv_project(kvshot_kvproj_handle h, int32_t n_tokens, int32_
     slot->has_combine = p.splits > 1;
     if (hipEventRecord(slot->ev[0], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   }
-  if (launch_kvproj(p, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
+  if ((pl.path == 2 ? launch_kvproj_direct(p, s) : launch_kvproj(p, s)) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (slot && hipEventRecord(slot->ev[1], s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (p.splits > 1 && launch_kvproj_combine(p, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   if (slot) {
@@ -298,6 +361,10 @@ kvshot_status kvshot_kvproj_set_option(kvshot_kvproj_handle h, int32_t option, i
       if (value < 0 || value > kProjMaxSplits) return KVSHOT_ERR_INVALID_ARG;
       h->opt_splits = (int)value;
       return KVSHOT_OK;
+    case KVSHOT_OPT_PATH:
+      if (value < 0 || value > 2) return KVSHOT_ERR_INVALID_ARG;
+      h->opt_path = (int)value;
+      return KVSHOT_OK;
     case KVSHOT_OPT_PROFILE:
       if (value != 0 && value != 1) return KVSHOT_ERR_INVALID_ARG;
       if (value && h->prof.empty()) {
@@ -319,11 +386,14 @@ kvshot_status kvshot_kvproj_set_option(kvshot_kvproj_handle h, int32_t option, i
   }
 }
 
-kvshot_status kvshot_kvproj_plan(kvshot_kvproj_handle h, int32_t n_tokens, int32_t* splits, int32_t* workgroups) {
+kvshot_status kvshot_kvproj_plan(kvshot_kvproj_handle h, int32_t n_tokens, int32_t* splits, int32_t* path,
+                                 int32_t* tile_tokens, int32_t* workgroups) {
   if (!h || n_tokens < 1 || n_tokens > h->cfg.max_tokens) return KVSHOT_ERR_INVALID_ARG;
-  const int s = plan_splits(h, n_tokens);
-  if (splits) *splits = s;
-  if (workgroups) *workgroups = 2 * m_tiles_of(h) * n_tiles_of(n_tokens) * s;
+  const ProjPlan pl = make_plan(h, n_tokens);
+  if (splits) *splits = pl.splits;
+  if (path) *path = pl.path;
+  if (tile_tokens) *tile_tokens = pl.path == 2 ? 16 * pl.tile16 : kProjTile;
+  if (workgroups) *workgroups = pl.workgroups;
   return KVSHOT_OK;
 }
 

@@ -14,6 +14,7 @@ constexpr int kProjTile = 256;        // output channels and tokens per workgrou
 constexpr int kProjMaxLayers = 4;
 constexpr int kProjMaxSplits = 16;
 constexpr int kProjWorkspaceRows = 8192;   // (split, token) rows of 2 d_kv floats
+constexpr int kProjDirectMaxTile16 = 4;  // direct kernel: at most 64 tokens per tile
 
 struct KvProjParams {
   const uint16_t* k_src[kProjMaxLayers];   // source K pools, stacking order
@@ -34,12 +35,14 @@ struct KvProjParams {
   int32_t n_tokens, batch, hkv, layers;
   int32_t page_shift, max_pages_per_seq, num_pages, dst_num_pages, max_position;
   int32_t m_tiles;                         // channel tiles: ceil(Hkv / 2)
-  int32_t n_tiles;                         // token tiles: ceil(n_tokens / 256)
+  int32_t n_tiles;                         // token tiles: ceil(n_tokens / 256), direct kernel ceil(n_tokens / (16 tile16))
   int32_t splits, work_items, rope_keys;
+  int32_t tile16;                          // direct kernel: tokens per tile / 16 (1 .. kProjDirectMaxTile16)
 };
 
 hipError_t launch_kvproj(const KvProjParams& p, hipStream_t s);
 hipError_t launch_kvproj_combine(const KvProjParams& p, hipStream_t s);
+hipError_t launch_kvproj_direct(const KvProjParams& p, hipStream_t s);
 hipError_t launch_kvproj_validate(const KvProjParams& p, int32_t* flag, hipStream_t s);
 
 }  // namespace kvshot

@@ -191,7 +191,7 @@ def test_kvproj_null_handle(lib):
     assert lib.kvshot_kv_project(None, 1, 1, None, None, *([None] * 8), 0, None) == 1
     assert lib.kvshot_kv_project_validate(None, 1, 1, None, None, None, None, None, None, None) == 1
     assert lib.kvshot_kvproj_set_option(None, 0, 0) == 1
-    assert lib.kvshot_kvproj_plan(None, 1, None, None) == 1
+    assert lib.kvshot_kvproj_plan(None, 1, None, None, None, None) == 1
     assert lib.kvshot_kvproj_profile_read(None, None, None, None) == 1
     assert lib.kvshot_kvproj_destroy(None) == 0
 

@@ -68,8 +68,9 @@ class Dev:
         return x.view(self.t.int16).cpu().numpy().view(np.uint16)
 
 
-def run(proj, case, dev, *, rope=True, splits=0):
+def run(proj, case, dev, *, rope=True, splits=0, path=0):
     proj.set_option(0, splits)
+    proj.set_option(1, path)
     proj(dev.k, dev.v, dev.table, dev.seq, dev.pos, dev.wk, dev.wv, dev.kd, dev.vd, dst_page_table=dev.dst_table,
          rope=rope)
     G.torch().cuda.synchronize()
@@ -110,33 +111,64 @@ def check(case, dev, kd, vd, *, rope, what, sample=None):
 
 
 @pytest.mark.parametrize("rope", [True, False])
-@pytest.mark.parametrize("splits", [0, 1, 2, 5, 16])
-def test_prefill_small_batch_matches_oracle(splits, rope):
+@pytest.mark.parametrize("path,splits", [(0, 0), (1, 0), (1, 1), (1, 2), (1, 5), (1, 16), (2, 0)])
+def test_prefill_small_batch_matches_oracle(path, splits, rope):
     c = W.kvproj_case(batch=3, ctx_lens=[300, 45, 17], new_tokens=[300, 45, 17], seed=11)
     dev = Dev(c)
     with handle(c) as proj:
-        kd, vd = run(proj, c, dev, rope=rope, splits=splits)
+        kd, vd = run(proj, c, dev, rope=rope, splits=splits, path=path)
         plan = proj.plan(c.n_tokens)
-    check(c, dev, kd, vd, rope=rope, what=f"prefill splits={splits} (plan {plan}) rope={rope}")
+    assert plan["path"] == (path or 2), plan     # 362 tokens: the tiled kernel would split, so auto is direct
+    check(c, dev, kd, vd, rope=rope, what=f"prefill path={path} splits={splits} (plan {plan}) rope={rope}")
 
 
-def test_verified_tokens_of_a_ragged_batch():
+@pytest.mark.parametrize("path", [0, 1])
+def test_verified_tokens_of_a_ragged_batch(path):
     c = W.kvproj_case(batch=4, ctx_lens=[1000, 64, 513, 7], new_tokens=[4, 1, 8, 7], seed=12)
     dev = Dev(c)
     with handle(c) as proj:
-        kd, vd = run(proj, c, dev)
-    check(c, dev, kd, vd, rope=True, what="verify ragged")
+        kd, vd = run(proj, c, dev, path=path)
+        plan = proj.plan(c.n_tokens)
+    check(c, dev, kd, vd, rope=True, what=f"verify ragged (plan {plan})")
 
 
-@pytest.mark.parametrize("hkv,layers", [(1, 3), (2, 1), (3, 2), (8, 4), (16, 1), (5, 3)])
-@pytest.mark.parametrize("splits", [0, 1])
-def test_head_counts_and_layer_counts(hkv, layers, splits):
+@pytest.mark.parametrize("counts", [[1], [40, 60], [100, 100], [64, 223], [240, 240], [7] * 64])
+def test_direct_path_tile_heights(counts):
+    # token counts whose direct plans take 16-, 32-, 48- and 64-token tiles (256 CUs), the last tile
+    # ragged; [7] * 64 is one verification of 64 sequences at 7 accepted tokens each
+    B = len(counts)
+    c = W.kvproj_case(batch=B, ctx_lens=[max(n, 1) + 37 * b for b, n in enumerate(counts)], new_tokens=counts,
+                      seed=30 + len(counts) + sum(counts))
+    dev = Dev(c)
+    with handle(c) as proj:
+        kd, vd = run(proj, c, dev, path=0)
+        plan = proj.plan(c.n_tokens)
+    assert plan["path"] == 2 and plan["splits"] == 1, plan
+    check(c, dev, kd, vd, rope=True, what=f"direct {c.n_tokens} tokens (plan {plan})")
+
+
+def test_direct_path_forced_on_a_large_call_sampled():
+    # 5000 tokens on the direct kernel: several workgroups per CU
+    c = W.kvproj_case(batch=2, ctx_lens=[3000, 2600], new_tokens=[3000, 2000], seed=21)
+    dev = Dev(c)
+    with handle(c) as proj:
+        kd, vd = run(proj, c, dev, path=2)
+        plan = proj.plan(c.n_tokens)
+    assert plan["path"] == 2 and plan["workgroups"] > 256, plan
+    rng = np.random.default_rng(21)
+    sample = np.concatenate([np.arange(200), rng.choice(c.n_tokens, 400, replace=False), [c.n_tokens - 1]])
+    check(c, dev, kd, vd, rope=True, what=f"direct forced, 5000 tokens (plan {plan})", sample=sample)
+
+
+@pytest.mark.parametrize("hkv,layers", [(1, 3), (2, 1), (3, 2), (8, 4), (16, 1), (5, 3), (1, 1)])
+@pytest.mark.parametrize("path,splits", [(2, 0), (1, 0), (1, 1)])
+def test_head_counts_and_layer_counts(hkv, layers, path, splits):
     c = W.kvproj_case(batch=2, ctx_lens=[130, 300], new_tokens=[130, 40], num_kv_heads=hkv, layers=layers,
                       seed=13 + hkv + 10 * layers)
     dev = Dev(c)
     with handle(c) as proj:
-        kd, vd = run(proj, c, dev, splits=splits)
-    check(c, dev, kd, vd, rope=True, what=f"Hkv={hkv} L={layers} splits={splits}")
+        kd, vd = run(proj, c, dev, splits=splits, path=path)
+    check(c, dev, kd, vd, rope=True, what=f"Hkv={hkv} L={layers} path={path} splits={splits}")
 
 
 def test_larger_pages_and_a_separate_destination_table():
@@ -167,17 +199,18 @@ def test_prefill_of_many_tiles_sampled():
     check(c, dev, kd, vd, rope=True, what="33k tokens (sampled)", sample=sample)
 
 
-def test_repeated_calls_are_bitwise_identical():
+@pytest.mark.parametrize("path", [1, 2])
+def test_repeated_calls_are_bitwise_identical(path):
     c = W.kvproj_case(batch=2, ctx_lens=[600, 90], new_tokens=[8, 90], seed=16)
     dev = Dev(c)
     with handle(c) as proj:
-        a = run(proj, c, dev)
-        b = run(proj, c, dev)
+        a = run(proj, c, dev, path=path)
+        b = run(proj, c, dev, path=path)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
-@pytest.mark.parametrize("splits", [1, 5])
-def test_hip_graph_replay_matches_eager(splits):
+@pytest.mark.parametrize("path,splits", [(1, 1), (1, 5), (2, 0)])
+def test_hip_graph_replay_matches_eager(path, splits):
     """A captured call replays to the eager result, with eager work and syncs between replays
     (split path: the combine kernel is captured too)."""
     t = G.torch()
@@ -185,6 +218,7 @@ def test_hip_graph_replay_matches_eager(splits):
     dev = Dev(c)
     with handle(c) as proj:
         proj.set_option(0, splits)
+        proj.set_option(1, path)
 
         def call():
             proj(dev.k, dev.v, dev.table, dev.seq, dev.pos, dev.wk, dev.wv, dev.kd, dev.vd, rope=True)
@@ -215,7 +249,7 @@ def test_hip_graph_replay_matches_eager(splits):
             assert np.array_equal(vd[pid, :, sl, :], ev[pid, :, sl, :]), rep
             call()                                  # eager work between replays
             t.cuda.synchronize()
-    check(c, dev, dev.host(eager_k), dev.host(eager_v), rope=True, what=f"graph splits={splits}")
+    check(c, dev, dev.host(eager_k), dev.host(eager_v), rope=True, what=f"graph path={path} splits={splits}")
 
 
 def test_validate_reports_the_first_bad_token():
@@ -269,6 +303,7 @@ def test_rejects_bad_arguments_before_queueing():
         assert call(wk=dev.wk.data_ptr() + 2) == 1      # misaligned
         assert call(kd=0) == 1
         assert lib.kvshot_kvproj_set_option(h, 0, 17) == 1
+        assert lib.kvshot_kvproj_set_option(h, 1, 3) == 1
         assert lib.kvshot_kvproj_set_option(h, 9, 0) == 1
         G.torch().cuda.synchronize()
         assert np.all(dev.host(dev.kd) == SENTINEL)
