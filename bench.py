@@ -205,6 +205,8 @@ def main():
                              "fusion_t64_d4096", "fusion_t480_d4096", "kvproj_prefill_b64_t32k",
                              "kvproj_verify_b64_t32k", "accept_n64m_k7", "treegrow_b8_v152k_d8k10n60"])
     ap.add_argument("--no-rope", action="store_true", help="--op kvproj: plain projection (no RoPE on keys)")
+    ap.add_argument("--fusion-tile", type=int, default=0, choices=[0, 1, 2],
+                    help="--op fusion: token tile, 0 automatic, 1 64 tokens, 2 128 tokens")
     ap.add_argument("--kvproj-path", type=int, default=0, choices=[0, 1, 2],
                     help="--op kvproj: 0 automatic, 1 the tiled kernel, 2 the direct kernel")
     ap.add_argument("--mode", choices=["folded", "sequential"], default="folded")
@@ -508,6 +510,8 @@ def bench_fusion(args, torch, K, W):
     fz = K.GatedDeltaFusion(d, tokens)
     if args.splits:
         fz.set_option(K.OPT_SPLITS, args.splits)
+    if args.fusion_tile:
+        fz.set_option(K.OPT_PATH, args.fusion_tile)
     plan = fz.plan(tokens)
     # weights are packed once, as a serving engine does at load time (outside the timed region)
     packed = None if args.fusion_row_major else fz.pack_weights(w_g, w_delta)
@@ -574,7 +578,7 @@ def bench_fusion(args, torch, K, W):
         roof = {"bound": "hbm", "achieved": round(main_bytes / (main_ms * 1e-3) / 1e9, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = read_fusion_traffic(name) if not args.splits else None
+    roof["traffic"] = read_fusion_traffic(name) if not (args.splits or args.fusion_tile) else None
     roof.update({"kernel": f"fusion_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)",
                  "kernel_ms": round(main_ms, 5), "combine_ms": round(comb_ms, 5),
                  "algorithmic_bytes_per_launch": main_bytes, "flops_per_launch": alg["flops"],

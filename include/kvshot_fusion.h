@@ -75,8 +75,12 @@ kvshot_status kvshot_gated_delta_fusion_packed(kvshot_fusion_handle h, int32_t t
                                                int32_t flags, void* stream);
 
 /* Options: KVSHOT_OPT_SPLITS (0 automatic, else 1, 2, 4, 8 or 16 workgroups
- * along the reduction; capped by the workspace) and KVSHOT_OPT_PROFILE (1: HIP events around each kernel of
- * every call), as for the attention handle. */
+ * along the reduction; capped by the workspace), KVSHOT_OPT_PATH (the token
+ * tile: 0 automatic -- 128 tokens per workgroup for calls of 256 tokens or
+ * more, else 64; 1 always 64; 2 always 128, except with 8 or 16 forced
+ * splits, which take 64) and KVSHOT_OPT_PROFILE (1: HIP events around each
+ * kernel of every call), as for the attention handle.  Every plan computes the
+ * same function; the split plan only changes the float32 summation order. */
 kvshot_status kvshot_fusion_set_option(kvshot_fusion_handle h, int32_t option, int64_t value);
 
 /* Plan of a call with `tokens` rows: reduction splits and workgroups of the

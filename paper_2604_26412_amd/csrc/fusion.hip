@@ -3,15 +3,19 @@
 // Sec. 3.4.1, Eqs. (delta) and (fusion), shapes from App. B ("Shared gate"):
 // for each draft token, Delta = o - n, g = sigmoid(W_g [n; o; Delta] + b_g)
 // and h = n + g * (W_Delta Delta).  The gate and the delta projection land on
-// the same output element, so one workgroup computes both for a tile of 64
-// tokens x 128 channels and applies the epilogue in registers.
+// the same output element, so one workgroup computes both for a tile of TT
+// tokens (64, or 128 for large token counts, where the bigger tile halves how
+// often each weight chunk is read from L2) x 128 channels and applies the
+// epilogue in registers.
 //
 // Reduction space: four segments of length d -- (n, W_g[:, 0:d]),
 // (o, W_g[:, d:2d]) and (Delta, W_g[:, 2d:3d]) into the gate accumulator,
 // (Delta, W_Delta) into the delta accumulator.  With few tokens (one draft
 // step of a batch) the segments, and then halves of them, are split over
-// workgroups so the grid still fills the chip; a second kernel sums the
-// split partials and applies the epilogue.
+// workgroups so the grid still fills the chip; with 128-token tiles the
+// reduction index range of all four segments is split instead (each split
+// reads only its part of n and o).  A second kernel sums the split partials
+// and applies the epilogue.
 //
 // Operands: activations are the A operand (rows = tokens).  They are staged
 // through LDS, where Delta is formed once per element (o - n in float32,
@@ -49,8 +53,6 @@ constexpr int kSteps = kKC / 16;                       // MFMA k-steps per chunk
 constexpr int kHalfSpan = kKC / 2;                     // reduction indices per lane half and chunk
 constexpr int kPitch = kKC + 8;                        // LDS row pitch (bf16): rows shift by 4 banks, so 16-byte row reads are conflict-free
 constexpr int kRowPieces = kKC / 8;                    // 16-byte pieces per activation row and chunk
-constexpr int kAPieces = kFusionTokens * kRowPieces / 256;   // pieces per thread and tensor
-constexpr int kTileElems = kFusionTokens * kPitch;     // one activation tile
 static_assert(kKC == 64 || kKC == 128, "chunk size");
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -69,13 +71,18 @@ __device__ __forceinline__ float sigmoidf_fast(float z) {
 }
 
 // NSEG: segments of the reduction space this workgroup covers (4: all of
-// them; 2 or 1 when split).  Segment i of a split is seg0 + i.  PF: chunks in
-// flight (activation and weight registers of each).
+// them; 2 or 1 when split).  Segment i of a split is seg0 + i; a split covers
+// the index range kbeg .. kbeg + d / kparts - 1 of its segments.  PF: chunks in
+// flight (activation and weight registers of each).  TT: tokens per tile.
 // WPS: workgroups per CU the register budget allows (a split kernel with one
 // segment is small enough for two, which hides each one's per-chunk latency).
-template <int NSEG, int PF, bool PACKED, int WPS>
+template <int NSEG, int PF, bool PACKED, int WPS, int TT>
 __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   static_assert(PF >= 2, "activations are staged one chunk ahead of the slot being computed");
+  static_assert(TT == 64 || TT == 128, "token tile");
+  constexpr int kAPieces = TT * kRowPieces / 256;       // pieces per thread and tensor
+  constexpr int kTileElems = TT * kPitch;              // one activation tile
+  constexpr int kTB = TT / 32;                         // 32-token MFMA blocks per tile
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][3][kTileElems];   // [buffer][n, o, Delta]
 
   const int tid = threadIdx.x;
@@ -89,9 +96,9 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   wi /= p.m_tiles;
   const int split = wi % p.splits;
   const int ntile = wi / p.splits;
-  const int m0 = mt * kFusionTokens;
+  const int m0 = mt * TT;
   const int d = p.d;
-  const int kparts = p.splits > 4 ? p.splits / 4 : 1;   // reduction-index parts per segment
+  const int kparts = p.kparts;                          // reduction-index parts per segment
   const int seg0 = NSEG == 4 ? 0 : (split / kparts) * NSEG;
   const int klen = d / kparts;
   const int kbeg = (split % kparts) * klen;
@@ -172,9 +179,11 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   // with a split, one per segment of the split.  Segment seg reads activation
   // tile min(seg, 2) (n, o, Delta) -- an address, not a branch.
   constexpr int NACC = NSEG == 4 ? 2 : NSEG;
-  f32x16 acc[NACC][2];
+  f32x16 acc[NACC][kTB];
 #pragma unroll
-  for (int a = 0; a < NACC; ++a) acc[a][0] = acc[a][1] = f32x16{};
+  for (int a = 0; a < NACC; ++a)
+#pragma unroll
+    for (int t = 0; t < kTB; ++t) acc[a][t] = f32x16{};
   int tile_of[NSEG];
 #pragma unroll
   for (int i = 0; i < NSEG; ++i) tile_of[i] = min(seg0 + i, 2) * kTileElems;
@@ -184,7 +193,7 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
 #pragma unroll
     for (int s = 0; s < kSteps; ++s) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < kTB; ++t) {
         const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh + 8 * s;
         if constexpr (NSEG == 4) {
           const bf16x8 a_n = as_bf16x8(*(const u32x4*)(base + off));
@@ -202,6 +211,9 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
           }
         }
       }
+      // 128-token tiles: keep the operand reads of one k-step together (hoisting a whole chunk's
+      // reads ahead of its products needs 192 more registers than a wave has)
+      if constexpr (TT == 128) __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -245,7 +257,7 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   const bool fused = p.splits == 1;
   const float bias = fused ? p.b_g[wc] : 0.0f;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < kTB; ++t) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int m = m0 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
@@ -321,13 +333,21 @@ __global__ __launch_bounds__(256) void fusion_combine_kernel(FusionParams p) {
 #define KVSHOT_FUSION_PF1 4
 #endif
 
+#ifndef KVSHOT_FUSION_PF4_TT128
+#define KVSHOT_FUSION_PF4_TT128 2
+#endif
+
 template <bool PACKED>
 void launch_fusion_t(const FusionParams& p, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)p.m_tiles * p.n_tiles * p.splits));
-  if (p.splits <= 1) hipLaunchKernelGGL((fusion_kernel<4, KVSHOT_FUSION_PF4, PACKED, 1>), grid, dim3(256), 0, s, p);
+  if (p.tile_tokens == 128) {   // every split covers all four segments (kparts == splits)
+    hipLaunchKernelGGL((fusion_kernel<4, KVSHOT_FUSION_PF4_TT128, PACKED, 1, 128>), grid, dim3(256), 0, s, p);
+    return;
+  }
+  if (p.splits <= 1) hipLaunchKernelGGL((fusion_kernel<4, KVSHOT_FUSION_PF4, PACKED, 1, 64>), grid, dim3(256), 0, s, p);
   else if (p.splits == 2)
-    hipLaunchKernelGGL((fusion_kernel<2, KVSHOT_FUSION_PF2, PACKED, 1>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((fusion_kernel<1, KVSHOT_FUSION_PF1, PACKED, 2>), grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((fusion_kernel<2, KVSHOT_FUSION_PF2, PACKED, 1, 64>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((fusion_kernel<1, KVSHOT_FUSION_PF1, PACKED, 2, 64>), grid, dim3(256), 0, s, p);
 }
 
 // One thread per 16-byte piece of the packed copy: it reads the 8 weights of

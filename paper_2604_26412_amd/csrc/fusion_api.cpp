@@ -26,7 +26,7 @@ struct kvshot_fusion_ctx {
   int d = 0, max_tokens = 0, device = 0, num_cus = 256;
   float* part = nullptr;
   size_t ws_pairs = 0;          // capacity of the partial workspace in (gate, delta) pairs of floats
-  int opt_splits = 0, opt_profile = 0;
+  int opt_splits = 0, opt_profile = 0, opt_tile = 0;
   std::vector<FusionProfileSlot> prof;
   int64_t prof_head = 0, prof_tail = 0;
   double main_ms = 0.0, combine_ms = 0.0;
@@ -37,24 +37,67 @@ namespace {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-int m_tiles_of(int tokens) { return (tokens + kFusionTokens - 1) / kFusionTokens; }
+int m_tiles_of(int tokens, int tile = kFusionTokens) { return (tokens + tile - 1) / tile; }
 
-// Reduction splits: the largest power of two (<= 8) that keeps the grid within
-// two workgroups per CU (two resident workgroups hide each other's per-chunk
-// latency: d = 4096, graph replay, 128 tokens 62 -> 50 us with 8 splits instead
-// of 4, 480 tokens 121 -> 107 us with 2 instead of 1, other sizes unchanged),
-// then capped by the workspace.  (16 splits measured slower: the larger partial
-// sum costs more in the combine than the main kernel gains.)
-int plan_splits(const kvshot_fusion_ctx* c, int tokens) {
-  const int64_t tiles = (int64_t)m_tiles_of(tokens) * (c->d / kFusionChannels);
+// Automatic plans consider 128-token tiles from this many tokens.
+constexpr int kFusionBigTileMin = 256;
+
+// The plan of a call: token tile, reduction splits and how a split divides the
+// reduction space.
+//  - 64-token tiles: the largest power of two (<= 8) that keeps the grid within
+//    two workgroups per CU (two resident workgroups hide each other's
+//    per-chunk latency: d = 4096, graph replay, 128 tokens 62 -> 50 us with 8
+//    splits instead of 4, 480 tokens 121 -> 107 us with 2 instead of 1, other
+//    sizes unchanged); splits take segments first (2: segments {0, 1} and
+//    {2, 3}; 4: one each), then halves of a segment (8).  16 splits measured
+//    slower: the larger partial sum costs more in the combine than the main
+//    kernel gains.
+//  - 128-token tiles: each weight chunk is read from L2 half as often.  The
+//    largest power of two (<= 4) that keeps the grid within one workgroup per
+//    CU (a 128-token workgroup holds a CU's registers); a split takes a part of
+//    the reduction index range of all four segments, so it reads only that
+//    part of n and o.  Automatic plans take them from kFusionBigTileMin tokens
+//    on where the 64-token grid would need a second round (one workgroup per CU
+//    unsplit, two split), or where it would split the reduction 4 ways or more
+//    while a 128-token grid covers every CU.  Measured at d = 4096 (main
+//    kernel, 64 -> 128-token tiles): 256 tokens 70.5 -> 57.6 us, 384 tokens
+//    86.0 -> 93.2 us, 480 tokens 96.0 -> 94.1 us (graph replay: step 113 ->
+//    116 us, the combine reading four planes instead of three), 640 to 1024
+//    tokens 224 -> 190 us.
+// Both capped by the workspace.
+struct FusionPlan {
+  int tile = kFusionTokens, splits = 1, kparts = 1, m_tiles = 0;
+};
+
+FusionPlan plan_tile(const kvshot_fusion_ctx* c, int tokens, int tile) {
+  FusionPlan pl;
+  const int64_t ntl = c->d / kFusionChannels;
+  pl.tile = tile;
+  pl.m_tiles = m_tiles_of(tokens, tile);
+  const int64_t tiles = (int64_t)pl.m_tiles * ntl;
   int s = 1;
-  if (c->opt_splits > 0) {
-    s = c->opt_splits;
-  } else {
+  if (c->opt_splits > 0) s = c->opt_splits;
+  else if (tile == 128)
+    while (s < 4 && tiles * s * 2 <= (int64_t)c->num_cus) s *= 2;
+  else
     while (s < 8 && tiles * s * 2 <= 2 * (int64_t)c->num_cus) s *= 2;
-  }
   while (s > 1 && (size_t)s * tokens * c->d > c->ws_pairs) s /= 2;
-  return s;
+  pl.splits = s;
+  pl.kparts = tile == 128 ? s : (s > 4 ? s / 4 : 1);
+  return pl;
+}
+
+FusionPlan make_plan(const kvshot_fusion_ctx* c, int tokens) {
+  const int64_t ntl = c->d / kFusionChannels;
+  const FusionPlan small = plan_tile(c, tokens, kFusionTokens);
+  if (c->opt_tile == 1 || c->opt_splits > 4) return small;
+  const FusionPlan big = plan_tile(c, tokens, 128);
+  if (c->opt_tile == 2) return big;
+  if (c->opt_splits > 0 || tokens < kFusionBigTileMin) return small;
+  const int64_t big_wgs = (int64_t)big.m_tiles * ntl * big.splits;
+  const int64_t small_wgs = (int64_t)small.m_tiles * ntl * small.splits;
+  const int64_t small_slots = (int64_t)c->num_cus * (small.splits > 1 ? 2 : 1);
+  return (small_wgs > small_slots || (big_wgs >= c->num_cus && small.splits >= 4)) ? big : small;
 }
 
 void free_fusion(kvshot_fusion_ctx* c) {
@@ -112,16 +155,18 @@ kvshot_status run_fusion(kvshot_fusion_handle h, int32_t tokens, const void* n, 
   p.part = h->part;
   p.tokens = tokens;
   p.d = h->d;
-  p.m_tiles = m_tiles_of(tokens);
+  const FusionPlan pl = make_plan(h, tokens);
+  p.m_tiles = pl.m_tiles;
   p.n_tiles = h->d / kFusionChannels;
-  p.splits = plan_splits(h, tokens);
+  p.splits = pl.splits;
+  p.kparts = pl.kparts;
+  p.tile_tokens = pl.tile;
   // which partial planes each split writes: split s covers segments [seg0, seg0 + nseg)
   // (segments 0-2 feed the gate, segment 3 the delta projection)
   {
-    const int nseg = p.splits >= 4 ? 1 : 4 / p.splits;
-    const int kparts = p.splits > 4 ? p.splits / 4 : 1;
+    const int nseg = 4 * pl.kparts / pl.splits;
     for (int sp = 0; sp < p.splits; ++sp) {
-      const int seg0 = (sp / kparts) * nseg;
+      const int seg0 = (sp / pl.kparts) * nseg;
       if (seg0 < 3) p.part_g_mask |= 1u << sp;
       if (seg0 + nseg > 3) p.part_d_mask |= 1u << sp;
     }
@@ -177,7 +222,7 @@ kvshot_status kvshot_fusion_init(int32_t d, int32_t max_tokens, kvshot_fusion_ha
   c->ws_pairs = (size_t)-1;
   for (int m = 1; m <= m_tiles_of(max_tokens); ++m) {
     const int tokens = m * kFusionTokens < max_tokens ? m * kFusionTokens : max_tokens;
-    const size_t s = (size_t)plan_splits(c, tokens);
+    const size_t s = (size_t)make_plan(c, tokens).splits;
     if (s > 1 && s * tokens * d > need) need = s * tokens * d;
   }
   c->ws_pairs = need;
@@ -228,6 +273,10 @@ kvshot_status kvshot_fusion_set_option(kvshot_fusion_handle h, int32_t option, i
         return KVSHOT_ERR_INVALID_ARG;
       h->opt_splits = (int)value;
       return KVSHOT_OK;
+    case KVSHOT_OPT_PATH:
+      if (value < 0 || value > 2) return KVSHOT_ERR_INVALID_ARG;
+      h->opt_tile = (int)value;
+      return KVSHOT_OK;
     case KVSHOT_OPT_PROFILE:
       if (value != 0 && value != 1) return KVSHOT_ERR_INVALID_ARG;
       if (value && h->prof.empty()) {
@@ -251,9 +300,9 @@ kvshot_status kvshot_fusion_set_option(kvshot_fusion_handle h, int32_t option, i
 
 kvshot_status kvshot_fusion_plan(kvshot_fusion_handle h, int32_t tokens, int32_t* splits, int32_t* workgroups) {
   if (!h || tokens < 1 || tokens > h->max_tokens) return KVSHOT_ERR_INVALID_ARG;
-  const int s = plan_splits(h, tokens);
-  if (splits) *splits = s;
-  if (workgroups) *workgroups = m_tiles_of(tokens) * (h->d / kFusionChannels) * s;
+  const FusionPlan pl = make_plan(h, tokens);
+  if (splits) *splits = pl.splits;
+  if (workgroups) *workgroups = pl.m_tiles * (h->d / kFusionChannels) * pl.splits;
   return KVSHOT_OK;
 }
 

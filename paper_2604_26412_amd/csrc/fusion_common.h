@@ -10,7 +10,7 @@
 
 namespace kvshot {
 
-constexpr int kFusionTokens = 64;     // tokens per fusion workgroup
+constexpr int kFusionTokens = 64;     // tokens per fusion workgroup (128 with the large-call tile)
 constexpr int kFusionChannels = 128;  // output channels per fusion workgroup
 constexpr int kFusionMaxSplits = 16;
 
@@ -28,6 +28,8 @@ struct FusionParams {
   uint32_t part_d_mask;         // bit s: split s contributes to the delta projection
   int32_t tokens, d;
   int32_t m_tiles, n_tiles, splits;
+  int32_t kparts;               // reduction-index parts of a segment: splits / (segment groups)
+  int32_t tile_tokens;          // tokens per workgroup tile: 64 or 128
   int32_t cross_only, out_fp32;
 };
 

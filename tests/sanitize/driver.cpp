@@ -196,8 +196,10 @@ static void fusion() {
   EXPECT(kvshot_fusion_init(4096, 0, &h) == KVSHOT_ERR_INVALID_ARG);
   EXPECT(kvshot_fusion_init(4096, 1024, &h) == KVSHOT_OK);
   if (!h) return;
-  for (int tokens : {1, 37, 64, 100, 480, 1024}) {
-    for (int splits : {0, 1, 2, 8}) {
+  for (int tile = 0; tile <= 2; ++tile)
+  for (int tokens : {1, 37, 64, 100, 256, 384, 480, 1024}) {
+    for (int splits : {0, 1, 2, 4, 8, 16}) {
+      EXPECT(kvshot_fusion_set_option(h, KVSHOT_OPT_PATH, tile) == KVSHOT_OK);
       EXPECT(kvshot_fusion_set_option(h, KVSHOT_OPT_SPLITS, splits) == KVSHOT_OK);
       int32_t s = 0, w = 0;
       EXPECT(kvshot_fusion_plan(h, tokens, &s, &w) == KVSHOT_OK);
@@ -207,6 +209,9 @@ static void fusion() {
                                               (float*)dev(), 0, nullptr) == KVSHOT_OK);
     }
   }
+  EXPECT(kvshot_fusion_set_option(h, KVSHOT_OPT_PATH, 0) == KVSHOT_OK);
+  EXPECT(kvshot_fusion_set_option(h, KVSHOT_OPT_SPLITS, 0) == KVSHOT_OK);
+  EXPECT(kvshot_fusion_set_option(h, KVSHOT_OPT_PATH, 3) == KVSHOT_ERR_INVALID_ARG);
   EXPECT(kvshot_fusion_pack_weights(h, dev(), dev(), dev(), nullptr) == KVSHOT_OK);
   EXPECT(kvshot_gated_delta_fusion(h, 1025, dev(), dev(), dev(), (const float*)dev(), dev(), dev(), nullptr, 0,
                                    nullptr) == KVSHOT_ERR_INVALID_ARG);

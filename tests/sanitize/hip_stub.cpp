@@ -144,7 +144,14 @@ hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int bl
   ++g_launches;
   return hipSuccess;
 }
-hipError_t launch_fusion(const FusionParams&, hipStream_t) {
+hipError_t launch_fusion(const FusionParams& p, hipStream_t) {
+  need(p.tile_tokens == 64 || p.tile_tokens == 128, "fusion tile");
+  need(p.m_tiles * p.tile_tokens >= p.tokens && (p.m_tiles - 1) * p.tile_tokens < p.tokens, "fusion token tiles");
+  need(p.splits >= 1 && p.kparts >= 1 && p.splits % p.kparts == 0 && (4 * p.kparts) % p.splits == 0, "fusion splits");
+  need((p.d / p.kparts) % 64 == 0, "fusion reduction parts");
+  need(p.tile_tokens == 64 || p.kparts == p.splits, "128-token tiles split the index range");
+  need(p.splits == 1 || p.part, "fusion partials");
+  need(p.w_packed || (p.w_g && p.w_delta), "fusion weights");
   ++g_launches;
   return hipSuccess;
 }

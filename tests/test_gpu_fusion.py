@@ -82,6 +82,57 @@ def test_fusion_matches_oracle(tokens, d, splits):
     assert np.max(np.abs(g - g_ref)) <= 5e-3
 
 
+@pytest.mark.parametrize("d", [256, 512])
+@pytest.mark.parametrize("tokens", [1, 100, 128, 200, 300])
+@pytest.mark.parametrize("splits", [0, 1, 2, 4])
+def test_fusion_128_token_tiles_match_oracle(tokens, d, splits):
+    # 128-token tiles (KVSHOT_OPT_PATH 2): splits take parts of the reduction index range of all four
+    # segments; ragged last tiles at 100, 200 and 300 tokens
+    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS, OPT_PATH
+    _log(f"fusion 128-token tiles tokens={tokens} d={d} splits={splits}")
+    c = W.fusion_case(tokens, d, seed=tokens * 11 + d + splits)
+    h_ref, g_ref = reference(c)
+    with GatedDeltaFusion(d, max(tokens, 64)) as fz:
+        fz.set_option(OPT_SPLITS, splits)
+        fz.set_option(OPT_PATH, 2)
+        plan = fz.plan(tokens)
+        assert plan["workgroups"] == -(-tokens // 128) * (d // 128) * plan["splits"], plan
+        h, g = run(fz, upload(c), c)
+    check(h, h_ref, False, f"h 128-token tiles tokens={tokens} d={d} splits={splits}")
+    assert np.max(np.abs(g - g_ref)) <= 5e-3
+
+
+@pytest.mark.parametrize("tokens", [256, 300, 480])
+def test_fusion_automatic_plan_at_large_token_counts(tokens):
+    from paper_2604_26412_amd import GatedDeltaFusion
+    c = W.fusion_case(tokens, 512, seed=tokens + 3)
+    h_ref, g_ref = reference(c)
+    with GatedDeltaFusion(512, tokens) as fz:
+        plan = fz.plan(tokens)
+        h, g = run(fz, upload(c), c)
+    check(h, h_ref, False, f"h automatic tokens={tokens} (plan {plan})")
+    assert np.max(np.abs(g - g_ref)) <= 5e-3
+
+
+@pytest.mark.parametrize("tile", [1, 2])
+def test_fusion_tiles_agree_with_packed_weights_and_fp32_output(tile):
+    from paper_2604_26412_amd import GatedDeltaFusion, OPT_PATH, OPT_SPLITS
+    t = G.torch()
+    c = W.fusion_case(150, 256, seed=41)
+    h_ref, g_ref = reference(c)
+    with GatedDeltaFusion(256, 150) as fz:
+        fz.set_option(OPT_PATH, tile)
+        dv = upload(c)
+        packed = fz.pack_weights(dv["w_g"], dv["w_delta"])
+        for splits in (1, 2):
+            fz.set_option(OPT_SPLITS, splits)
+            a = fz(dv["n"], dv["o"], dv["w_g"], dv["b_g"], dv["w_delta"], out_dtype="fp32")
+            b = fz(dv["n"], dv["o"], None, dv["b_g"], None, packed=packed, out_dtype="fp32")
+            t.cuda.synchronize()
+            assert t.equal(a, b), (tile, splits)
+            check(a.cpu().numpy(), h_ref, True, f"fp32 tile {64 * tile} splits {splits}")
+
+
 @pytest.mark.parametrize("splits", [1, 8])
 def test_fusion_float32_output_and_gate(splits):
     from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS
@@ -94,14 +145,16 @@ def test_fusion_float32_output_and_gate(splits):
     assert np.max(np.abs(g - g_ref)) <= 5e-3
 
 
+@pytest.mark.parametrize("tile", [1, 2])
 @pytest.mark.parametrize("splits", [1, 4])
-def test_fusion_cross_only(splits):
+def test_fusion_cross_only(splits, tile):
     # reading: the cross-only variant drops n (n = 0, Delta = o)
-    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS
+    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS, OPT_PATH
     c = W.fusion_case(50, 256, seed=6)
     h_ref, g_ref = reference(c, cross_only=True)
     with GatedDeltaFusion(256, 64) as fz:
         fz.set_option(OPT_SPLITS, splits)
+        fz.set_option(OPT_PATH, tile)
         h, g = run(fz, upload(c), c, cross_only=True)
     check(h, h_ref, False, f"cross-only splits={splits}")
     assert np.max(np.abs(g - g_ref)) <= 5e-3
@@ -140,15 +193,16 @@ def test_fusion_is_deterministic_and_split_invariant():
     assert np.max(np.abs(outs[1] - outs[8])) <= 1e-4 * (1 + np.max(np.abs(outs[1])))
 
 
-@pytest.mark.parametrize("splits", [1, 8])
-def test_fusion_hip_graph_replay_matches_eager(splits):
+@pytest.mark.parametrize("splits,tile", [(1, 1), (8, 1), (2, 2)])
+def test_fusion_hip_graph_replay_matches_eager(splits, tile):
     """A captured call replays to the eager result, with eager work and syncs between replays
     (split path: the combine kernel is captured too)."""
-    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS
+    from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS, OPT_PATH
     t = G.torch()
     c = W.fusion_case(64, 512, seed=19)
     with GatedDeltaFusion(512, 64) as fz:
         fz.set_option(OPT_SPLITS, splits)
+        fz.set_option(OPT_PATH, tile)
         dv = upload(c)
         out = t.empty((c.tokens, c.d), dtype=t.bfloat16, device="cuda")
         gate = t.empty((c.tokens, c.d), dtype=t.float32, device="cuda")
