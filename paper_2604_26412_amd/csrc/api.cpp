@@ -42,7 +42,7 @@ struct kvshot_ctx {
   float* part_o = nullptr;
   float2* part_ml = nullptr;
   int32_t* flag = nullptr;
-  int32_t* seq_splits = nullptr;   // [64]: per-sequence split counts of a balanced call
+  int32_t* seq_splits = nullptr;   // [2][64]: per-sequence split counts and first items of a balanced call
   size_t ws_rows = 0;       // capacity of the partial workspace in (row, split) entries
   int opt_splits = 0, opt_path = 0, opt_profile = 0;
   std::vector<ProfileSlot> prof;
@@ -144,19 +144,22 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_t
   if (pl.path == 3 && bps > tall_max_blocks()) return make_plan(c, batch, nq, max_ctx, false);
   pl.splits = splits;
   pl.blocks_per_split = bps;
-  // Ragged batches on the general MFMA kernel: share one round of work items per KV head out over
-  // the sequences in proportion to their lengths (computed on the device from ctx_lens), instead
-  // of giving every sequence the same split count.  Only when the items outnumber the sequences.
-  if (pl.path == 1 && c->opt_splits == 0 && batch >= 2 && batch <= 64) {
-    const int per_cu = mfma_wgs_per_cu(pl.kernel_row_tiles);
-    int items = c->num_cus * per_cu / (c->cfg.num_kv_heads * pl.row_groups);
-    if (items > c->max_splits) items = c->max_splits;
-    while (items > 1 && (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * items > c->ws_rows) --items;
+  // Ragged batches of 32-row tiles on the general MFMA kernel: one-wave workgroups, one round of
+  // them over the chip (four per CU), shared out as work items per KV head over the sequences in
+  // proportion to their lengths (computed on the device from ctx_lens), instead of giving every
+  // sequence the same split count.  With four times the items of four-wave workgroups, a sequence's
+  // whole-number share of them is four times finer.  Only when the items outnumber the sequences.
+  if (pl.path == 1 && pl.kernel_row_tiles == 1 && c->opt_splits == 0 && batch >= 2 && batch <= 64) {
+    const int per_cu = mfma_wgs_per_cu(1) * mfma_waves_per_wg(1);   // one-wave workgroups per CU
+    int items = c->num_cus * per_cu / c->cfg.num_kv_heads;
+    while (items > 1 && (size_t)c->cfg.num_kv_heads * pl.rows_pad * items > c->ws_rows) --items;
     if (items > batch) {
       pl.balanced = 1;
       pl.items = items;
-      pl.min_chunk = pl.key_streams * 2;
-      pl.splits = items;              // a sequence has at most `items` splits: the partials' stride
+      pl.min_chunk = 1;
+      pl.waves_per_wg = 1;
+      pl.key_streams = 1;
+      pl.splits = items;              // the grid's items per KV head; a sequence takes at most kMaxSplits
       pl.blocks_per_split = 0;
     }
   }
@@ -313,6 +316,7 @@ kvshot_status run_call(kvshot_ctx* c, const kvshot_call& a, void* stream, const 
     cp.splits = pl.splits;
     cp.out_fp32 = g.out_dtype == KVSHOT_FP32;
     cp.seq_splits = pl.balanced ? p.seq_splits : nullptr;
+    cp.items = pl.balanced ? pl.items : 0;
     if (launch_combine(cp, s) != hipSuccess) return KVSHOT_ERR_DEVICE;
   }
   if (slot) {
@@ -391,17 +395,24 @@ void* scratch_ptr(int device) {
   return g_scratch_ptr[device];
 }
 
-// Scratch bytes a plan uses: split partials O [batch][Hkv][rows_pad][splits][D] float32, then
-// (m, l) [batch][Hkv][rows_pad][splits] float2, then the 64 per-sequence split counts of a
-// balanced plan, each at the next 256-byte boundary.
+// Scratch bytes a plan uses: split partials O float32 ([batch][Hkv][rows_pad][splits], or
+// [Hkv][items][rows_pad] under the balanced schedule) x D, then (m, l) float2 per partial row, then
+// the per-sequence split counts and first items of a balanced plan ([2][64] int32), each at the
+// next 256-byte boundary.
+size_t partial_rows(const kvshot_ctx* c, const Plan& pl, int batch) {
+  if (pl.splits <= 1) return 0;
+  if (pl.balanced) return (size_t)c->cfg.num_kv_heads * pl.items * pl.rows_pad;
+  return (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * pl.splits;
+}
+
 size_t partial_bytes(const kvshot_ctx* c, const Plan& pl, int batch, size_t* ml_offset, size_t* seq_offset) {
   *ml_offset = 0;
   *seq_offset = 0;
   if (pl.splits <= 1) return 0;
-  const size_t rows = (size_t)batch * c->cfg.num_kv_heads * pl.rows_pad * pl.splits;
+  const size_t rows = partial_rows(c, pl, batch);
   *ml_offset = (rows * kHeadDim * sizeof(float) + 255) & ~(size_t)255;
   *seq_offset = (*ml_offset + rows * sizeof(float2) + 255) & ~(size_t)255;
-  return *seq_offset + (pl.balanced ? 64 * sizeof(int32_t) : 0);
+  return *seq_offset + (pl.balanced ? 2 * 64 * sizeof(int32_t) : 0);
 }
 
 void free_ctx(kvshot_ctx* c) {
@@ -496,7 +507,7 @@ kvshot_status kvshot_draft_attn_init(const kvshot_config* cfg, kvshot_handle* ou
       hipMalloc((void**)&c->part_o, c->ws_rows * kHeadDim * sizeof(float)) != hipSuccess ||
       hipMalloc((void**)&c->part_ml, c->ws_rows * sizeof(float2)) != hipSuccess ||
       hipMalloc((void**)&c->flag, sizeof(int32_t)) != hipSuccess ||
-      hipMalloc((void**)&c->seq_splits, 64 * sizeof(int32_t)) != hipSuccess) {
+      hipMalloc((void**)&c->seq_splits, 2 * 64 * sizeof(int32_t)) != hipSuccess) {
     (void)hipGetLastError();
     free_ctx(c);
     return KVSHOT_ERR_OUT_OF_MEMORY;

@@ -570,7 +570,8 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
       if (p.lse && hh == 0)
         p.lse[((int64_t)b * p.nq + jrow[i]) * p.hq + hqr[i]] = (M[i] + __log2f(l_row[i])) * kLn2;
     } else {
-      const int64_t prow = (((int64_t)b * p.hkv + h) * p.rows_pad + r[i]) * p.splits + part;
+      const int64_t prow = p.balanced ? ((int64_t)h * p.items + item) * p.rows_pad + r[i]
+                                      : (((int64_t)b * p.hkv + h) * p.rows_pad + r[i]) * p.splits + part;
       float* po = p.part_o + prow * kHeadDim;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
@@ -604,11 +605,15 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
   if (own == 0) return;                            // past the last split of the batch (whole workgroup)
   const int b = __builtin_amdgcn_readfirstlane(__builtin_ctzll(own));
   const int nsplit = __builtin_amdgcn_readfirstlane(__shfl(sl.splits, b));
-  const int split = item - __builtin_amdgcn_readfirstlane(__shfl(sl.first, b));
+  const int first = __builtin_amdgcn_readfirstlane(__shfl(sl.first, b));
+  const int split = item - first;
   const int per = __builtin_amdgcn_readfirstlane(__shfl(sl.per, b));
   const int T = __builtin_amdgcn_readfirstlane(__shfl(sl.ctx, b));
-  // the combine reads each sequence's split count (one writer per sequence)
-  if (split == 0 && h == 0 && rg == 0 && threadIdx.x == 0) p.seq_splits[b] = nsplit;
+  // the combine reads each sequence's split count and first item (one writer per sequence)
+  if (split == 0 && h == 0 && rg == 0 && threadIdx.x == 0) {
+    p.seq_splits[b] = nsplit;
+    p.seq_splits[64 + b] = first;
+  }
   const int nbt = (T + kBlockKeys - 1) / kBlockKeys;
   segment(b, T, split, nsplit, split * per, min(split * per + per, nbt), split == nsplit - 1);
 }
@@ -621,6 +626,10 @@ __global__ __launch_bounds__(NW * 64, WPS) void attn_mfma_kernel(AttnParams p) {
 #endif
 #ifndef KVSHOT_RT1_PF
 #define KVSHOT_RT1_PF 1
+#endif
+// one-wave workgroups of the balanced schedule: blocks in flight per wave
+#ifndef KVSHOT_BAL_PF
+#define KVSHOT_BAL_PF 1
 #endif
 #ifndef KVSHOT_QSPLIT_MAX_RT
 #define KVSHOT_QSPLIT_MAX_RT 8
@@ -682,7 +691,11 @@ hipError_t launch_attn_mfma(const AttnParams& p, int kernel_row_tiles, hipStream
                  q8 = KVSHOT_QSPLIT_MAX_RT >= 8;
   switch (kernel_row_tiles) {
     case 1:
-      hipLaunchKernelGGL((attn_mfma_kernel<1, 1, 4, KVSHOT_RT1_PF, q1, KVSHOT_RT1_WPS>), grid, dim3(256), 0, s, p);
+      // balanced schedule: one-wave workgroups, each wave its own item (four items per CU)
+      if (p.balanced)
+        hipLaunchKernelGGL((attn_mfma_kernel<1, 1, 1, KVSHOT_BAL_PF, q1, KVSHOT_RT1_WPS>), grid, dim3(64), 0, s, p);
+      else
+        hipLaunchKernelGGL((attn_mfma_kernel<1, 1, 4, KVSHOT_RT1_PF, q1, KVSHOT_RT1_WPS>), grid, dim3(256), 0, s, p);
       break;
     case 2:
       hipLaunchKernelGGL((attn_mfma_kernel<2, 1, 4, KVSHOT_RT2_PF, q2, KVSHOT_RT24_WPS>), grid, dim3(256), 0, s, p);

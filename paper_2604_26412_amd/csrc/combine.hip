@@ -14,8 +14,9 @@ namespace {
 // row's result is sum_s O_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s,
 // the softmax-weighted sum over the union of the splits' keys; splits that saw
 // no key (l_s = 0) carry no weight.
-__device__ __forceinline__ void combine_row(const float* part_o, const float2* part_ml, int64_t base, int splits,
-                                            void* out, int64_t orow, bool out_fp32, float* lse_out, int lane) {
+__device__ __forceinline__ void combine_row(const float* part_o, const float2* part_ml, int64_t base, int64_t stride,
+                                            int splits, void* out, int64_t orow, bool out_fp32, float* lse_out,
+                                            int lane) {
   // Eight splits' rows are loaded at once, with no branch between them, so
   // their latencies overlap (the first eight also with the (m, l) load); a
   // split of weight zero is skipped by a select, so whatever its row holds
@@ -25,13 +26,13 @@ __device__ __forceinline__ void combine_row(const float* part_o, const float2* p
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int s = s0 + u < splits ? s0 + u : splits - 1;
-      v[u] = *(const float2*)(part_o + (base + s) * kHeadDim + lane * 2);
+      v[u] = *(const float2*)(part_o + (base + s * stride) * kHeadDim + lane * 2);
     }
   };
   load_rows(0);
   float ms = -INFINITY, ls = 0.0f;
   if (lane < splits) {
-    const float2 t = part_ml[base + lane];
+    const float2 t = part_ml[base + lane * stride];
     ms = t.y > 0.0f ? t.x : -INFINITY;
     ls = t.y;
   }
@@ -74,15 +75,20 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int hq = h * p.group + (r - j * p.group);
   const int64_t q_index = ((int64_t)b * p.nq + j) * p.hq + hq;
   int splits = p.splits;
+  int64_t base = (bh * p.rows_pad + r) * p.splits, stride = 1;
   if (p.seq_splits) {
-    // this sequence's split count under the attention kernel's balanced schedule; with one split the
-    // attention kernel wrote the output itself
+    // this sequence's split count and first item under the attention kernel's balanced schedule (its
+    // items' partials sit rows_pad rows apart); with one split the attention kernel wrote the output
     splits = p.seq_splits[b];
     if (splits <= 1) return;
-    splits = splits > p.splits ? p.splits : splits;
+    splits = splits > kMaxSplits ? kMaxSplits : splits;
+    int first = p.seq_splits[64 + b];
+    first = first < 0 ? 0 : (first > p.items - splits ? p.items - splits : first);
+    base = ((int64_t)h * p.items + first) * p.rows_pad + r;
+    stride = p.rows_pad;
   }
-  combine_row(p.part_o, p.part_ml, (bh * p.rows_pad + r) * p.splits, splits, p.out, q_index * kHeadDim,
-              p.out_fp32 != 0, p.lse ? p.lse + q_index : nullptr, lane);
+  combine_row(p.part_o, p.part_ml, base, stride, splits, p.out, q_index * kHeadDim, p.out_fp32 != 0,
+              p.lse ? p.lse + q_index : nullptr, lane);
 }
 
 }  // namespace

@@ -46,13 +46,14 @@ struct AttnParams {
   int32_t n_nodes;              // tree mode: draft-tree nodes (draft keys) per sequence
   int32_t out_fp32;
   float qscale;                 // softmax scale * log2(e): scores come out in log2 units
-  // Length-balanced schedule (batch <= 64): `items` work items per (KV head, row group) are shared
-  // out over the sequences in proportion to their lengths (balanced_schedule); `splits` is then
-  // the stride of a sequence's partials, an upper bound of its split count.
+  // Length-balanced schedule (batch <= 64, 32-row tiles, one-wave workgroups): `items` work items
+  // per KV head are shared out over the sequences in proportion to their lengths
+  // (balanced_schedule).  Item i of KV head h writes its partial at rows ((h * items + i) *
+  // rows_pad + r); a sequence's items are consecutive.
   int32_t balanced;
   int32_t items;
-  int32_t min_chunk;            // blocks per item at least (a multiple of the key streams)
-  int32_t* seq_splits;          // [batch]: each sequence's split count, written for the combine
+  int32_t min_chunk;            // blocks per item at least
+  int32_t* seq_splits;          // [2][64]: each sequence's split count, then its first item, for the combine
 };
 
 struct CombineParams {
@@ -61,8 +62,10 @@ struct CombineParams {
   void* out;
   float* lse;
   int32_t batch, nq, hq, hkv, group, rows, rows_pad, splits, out_fp32;
-  // balanced schedule: each sequence's split count, written by the attention kernel (null: `splits`)
+  // balanced schedule: each sequence's split count and first item ([2][64]), written by the attention
+  // kernel, and the items per KV head (null / 0: every sequence has `splits` splits)
   const int32_t* seq_splits;
+  int32_t items;
 };
 
 // ---------------------------------------------------------------------------
@@ -144,6 +147,31 @@ struct BalancedSlot {
   int per;      // its blocks per split
   int first;    // exclusive prefix of split counts
 };
+// Wave-wide sum and prefix of small non-negative per-lane values (< 2^bits) from
+// bit-plane ballots: no cross-lane data movement through LDS, so no LDS latency
+// on the chain.
+__device__ __forceinline__ int wave_sum_small(int v, int bits) {
+  int total = 0;
+  for (int bit = 0; bit < bits; ++bit) total += __popcll(__ballot((v >> bit) & 1)) << bit;
+  return total;
+}
+__device__ __forceinline__ int wave_exclusive_prefix_small(int v, int bits, int lane) {
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));   // lanes < lane
+  int pre = 0;
+  for (int bit = 0; bit < bits; ++bit) pre += __popcll(__ballot((v >> bit) & 1) & below) << bit;
+  return pre;
+}
+
+// ceil(a / c) for 0 <= a <= 2^25 and uniform c >= 1: a float reciprocal estimate (within one of the
+// quotient at these sizes), corrected by one
+__device__ __forceinline__ int ceil_div_small(int a, int c, float rc) {
+  const int num = a + c - 1;
+  int q = (int)((float)num * rc);
+  if (q * c > num) --q;
+  else if ((q + 1) * c <= num) ++q;
+  return q;
+}
+
 __device__ __forceinline__ BalancedSlot balanced_schedule(const int32_t* ctx_lens, int batch, int max_ctx,
                                                           int max_pages_per_seq, int page_shift, int items,
                                                           int min_chunk, int lane) {
@@ -153,14 +181,18 @@ __device__ __forceinline__ BalancedSlot balanced_schedule(const int32_t* ctx_len
     t = t > max_ctx ? max_ctx : t;
     nb = (t + kBlockKeys - 1) / kBlockKeys;
   }
-  int maxnb = nb;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) maxnb = max(maxnb, __shfl_xor(maxnb, o));
+  // the longest prefix, by a bit-serial wave max (block counts <= 2^25: prefixes <= 2^30 keys)
+  int maxnb = 0;
+  for (int bit = 25; bit >= 0; --bit) {
+    const int cand = maxnb | (1 << bit);
+    if (__ballot(nb >= cand)) maxnb = cand;
+  }
+  // a sequence takes at most kMaxSplits items (what the combine merges)
+  auto splits_of = [&](int chunk, float rc) {
+    return lane < batch ? min(kMaxSplits, max(1, ceil_div_small(nb, chunk, rc))) : 0;
+  };
   auto total_splits = [&](int chunk) {
-    int v = lane < batch ? max(1, (nb + chunk - 1) / chunk) : 0;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    return wave_sum_small(splits_of(chunk, 1.0f / (float)chunk), 7);
   };
   // chunk = min_chunk * k: the smallest k in [1, kmax] that fits (kmax covers the longest prefix)
   const int kmax = max(1, (maxnb + min_chunk - 1) / min_chunk);
@@ -173,15 +205,9 @@ __device__ __forceinline__ BalancedSlot balanced_schedule(const int32_t* ctx_len
   const int chunk = lo * min_chunk;
   BalancedSlot r;
   r.ctx = t;
-  r.splits = lane < batch ? max(1, (nb + chunk - 1) / chunk) : 0;
+  r.splits = splits_of(chunk, 1.0f / (float)chunk);
   r.per = lane < batch ? (nb + r.splits - 1) / r.splits : 0;
-  int incl = r.splits;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
-  }
-  r.first = incl - r.splits;
+  r.first = wave_exclusive_prefix_small(r.splits, 7, lane);
   return r;
 }
 
