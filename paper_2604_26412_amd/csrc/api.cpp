@@ -148,12 +148,15 @@ Plan make_plan(const kvshot_ctx* c, int batch, int nq, int max_ctx, bool allow_t
   // them over the chip (four per CU), shared out as work items per KV head over the sequences in
   // proportion to their lengths (computed on the device from ctx_lens), instead of giving every
   // sequence the same split count.  With four times the items of four-wave workgroups, a sequence's
-  // whole-number share of them is four times finer.  Only when the items outnumber the sequences.
+  // whole-number share of them is four times finer.  Only for batches of at most a quarter as many
+  // sequences as items: larger batches fill the chip with one workgroup per (sequence, KV head) and
+  // their unsplit plan needs no partials and no combine (64 x 32K: the balanced plan's combine adds
+  // 16 us to a 1.26 ms step).
   if (pl.path == 1 && pl.kernel_row_tiles == 1 && c->opt_splits == 0 && batch >= 2 && batch <= 64) {
     const int per_cu = mfma_wgs_per_cu(1) * mfma_waves_per_wg(1);   // one-wave workgroups per CU
     int items = c->num_cus * per_cu / c->cfg.num_kv_heads;
     while (items > 1 && (size_t)c->cfg.num_kv_heads * pl.rows_pad * items > c->ws_rows) --items;
-    if (items > batch) {
+    if (4 * batch <= items) {
       pl.balanced = 1;
       pl.items = items;
       pl.min_chunk = 1;
