@@ -188,32 +188,50 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
 #pragma unroll
   for (int i = 0; i < NSEG; ++i) tile_of[i] = min(seg0 + i, 2) * kTileElems;
 
+  // Fragments of one k-step: [32-token block][tensor read] (all four segments: n, o and Delta, the
+  // last one feeding both accumulators; a split: one read per segment).
+  constexpr int NF = NSEG == 4 ? 3 : NSEG;
+  auto read_frags = [&](const uint16_t* base, int s, bf16x8 (&f)[kTB][NF]) {
+#pragma unroll
+    for (int t = 0; t < kTB; ++t) {
+      const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh + 8 * s;
+      if constexpr (NSEG == 4) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) f[t][j] = as_bf16x8(*(const u32x4*)(base + j * kTileElems + off));
+      } else {
+#pragma unroll
+        for (int i = 0; i < NSEG; ++i) f[t][i] = as_bf16x8(*(const u32x4*)(base + tile_of[i] + off));
+      }
+    }
+  };
+  auto mfmas = [&](int s, const bf16x8 (&f)[kTB][NF], const u32x4 (&wr)[NSEG][kSteps]) {
+#pragma unroll
+    for (int t = 0; t < kTB; ++t) {
+      if constexpr (NSEG == 4) {
+        acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][0], as_bf16x8(wr[0][s]), acc[0][t], 0, 0, 0);
+        acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][1], as_bf16x8(wr[1][s]), acc[0][t], 0, 0, 0);
+        acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][2], as_bf16x8(wr[2][s]), acc[0][t], 0, 0, 0);
+        acc[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][2], as_bf16x8(wr[3][s]), acc[1][t], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int i = 0; i < NSEG; ++i)
+          acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][i], as_bf16x8(wr[i][s]), acc[i][t], 0, 0, 0);
+      }
+    }
+  };
+  // One chunk from LDS buffer buf.  The operand reads of k-step s + 1 are issued before the
+  // products of k-step s (scheduling barriers keep them there), so their LDS latency hides behind
+  // the matrix core instead of stalling each product on a read issued just before it.
   auto compute = [&](int buf, const u32x4 (&wr)[NSEG][kSteps]) {
     const uint16_t* base = &lds[buf][0][0];
+    bf16x8 f[2][kTB][NF];
+    read_frags(base, 0, f[0]);
 #pragma unroll
     for (int s = 0; s < kSteps; ++s) {
-#pragma unroll
-      for (int t = 0; t < kTB; ++t) {
-        const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh + 8 * s;
-        if constexpr (NSEG == 4) {
-          const bf16x8 a_n = as_bf16x8(*(const u32x4*)(base + off));
-          const bf16x8 a_o = as_bf16x8(*(const u32x4*)(base + kTileElems + off));
-          const bf16x8 a_d = as_bf16x8(*(const u32x4*)(base + 2 * kTileElems + off));
-          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_n, as_bf16x8(wr[0][s]), acc[0][t], 0, 0, 0);
-          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_o, as_bf16x8(wr[1][s]), acc[0][t], 0, 0, 0);
-          acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_d, as_bf16x8(wr[2][s]), acc[0][t], 0, 0, 0);
-          acc[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_d, as_bf16x8(wr[3][s]), acc[1][t], 0, 0, 0);
-        } else {
-#pragma unroll
-          for (int i = 0; i < NSEG; ++i) {
-            const bf16x8 a = as_bf16x8(*(const u32x4*)(base + tile_of[i] + off));
-            acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(wr[i][s]), acc[i][t], 0, 0, 0);
-          }
-        }
-      }
-      // 128-token tiles: keep the operand reads of one k-step together (hoisting a whole chunk's
-      // reads ahead of its products needs 192 more registers than a wave has)
-      if constexpr (TT == 128) __builtin_amdgcn_sched_barrier(0);
+      if (s + 1 < kSteps) read_frags(base, s + 1, f[(s + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(s, f[s & 1], wr);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -334,7 +352,7 @@ __global__ __launch_bounds__(256) void fusion_combine_kernel(FusionParams p) {
 #endif
 
 #ifndef KVSHOT_FUSION_PF4_TT128
-#define KVSHOT_FUSION_PF4_TT128 2
+#define KVSHOT_FUSION_PF4_TT128 3
 #endif
 
 template <bool PACKED>

@@ -57,13 +57,9 @@ constexpr int kFusionBigTileMin = 256;
 //    CU (a 128-token workgroup holds a CU's registers); a split takes a part of
 //    the reduction index range of all four segments, so it reads only that
 //    part of n and o.  Automatic plans take them from kFusionBigTileMin tokens
-//    on where the 64-token grid would need a second round (one workgroup per CU
-//    unsplit, two split), or where it would split the reduction 4 ways or more
-//    while a 128-token grid covers every CU.  Measured at d = 4096 (main
-//    kernel, 64 -> 128-token tiles): 256 tokens 70.5 -> 57.6 us, 384 tokens
-//    86.0 -> 93.2 us, 480 tokens 96.0 -> 94.1 us (graph replay: step 113 ->
-//    116 us, the combine reading four planes instead of three), 640 to 1024
-//    tokens 224 -> 190 us.
+//    on.  Measured at d = 4096 (main kernel + combine, 64 -> 128-token tiles):
+//    256 tokens 75 -> 65 us, 384 tokens 97 -> 97 us, 480 tokens 107 -> 98 us,
+//    640 to 1024 tokens 216 -> 178 us.
 // Both capped by the workspace.
 struct FusionPlan {
   int tile = kFusionTokens, splits = 1, kparts = 1, m_tiles = 0;
@@ -88,16 +84,11 @@ FusionPlan plan_tile(const kvshot_fusion_ctx* c, int tokens, int tile) {
 }
 
 FusionPlan make_plan(const kvshot_fusion_ctx* c, int tokens) {
-  const int64_t ntl = c->d / kFusionChannels;
   const FusionPlan small = plan_tile(c, tokens, kFusionTokens);
   if (c->opt_tile == 1 || c->opt_splits > 4) return small;
   const FusionPlan big = plan_tile(c, tokens, 128);
   if (c->opt_tile == 2) return big;
-  if (c->opt_splits > 0 || tokens < kFusionBigTileMin) return small;
-  const int64_t big_wgs = (int64_t)big.m_tiles * ntl * big.splits;
-  const int64_t small_wgs = (int64_t)small.m_tiles * ntl * small.splits;
-  const int64_t small_slots = (int64_t)c->num_cus * (small.splits > 1 ? 2 : 1);
-  return (small_wgs > small_slots || (big_wgs >= c->num_cus && small.splits >= 4)) ? big : small;
+  return c->opt_splits > 0 || tokens < kFusionBigTileMin ? small : big;
 }
 
 void free_fusion(kvshot_fusion_ctx* c) {
