@@ -59,8 +59,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // Barrier without the memory fence of __syncthreads (which would also wait for
-// the ring loads still in flight); the clobber keeps LDS accesses on their side.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// the ring loads still in flight).  The wave's own LDS reads complete first, so
+// that no read of a ring buffer is still in flight when the barrier lets its
+// refill start; the clobber keeps LDS accesses on their side.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -441,6 +443,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_tall_kernel(AttnParams p) {
         for (int i = 0; i < TPW; ++i)
           oacc[i][dt] =
               __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][sidx], as_bf16x8(pw[i][sidx]), oacc[i][dt], 0, 0, 0);
+    // every V^T read issued before the first product, so one LDS latency is exposed instead of four
+    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8 * TPW, 0);
   };
 
   if (ntot > 0) {

@@ -72,9 +72,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // Barrier without the memory fence of __syncthreads (which would also wait for
-// the operand prefetches still in flight); the clobber keeps the compiler from
-// moving LDS accesses across it.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// the operand prefetches still in flight).  The wave's own LDS reads complete
+// first, so that no read of a ring stage is still in flight when the barrier
+// lets its refill start; the clobber keeps the compiler from moving LDS
+// accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // One wave-wide 16-byte load from global memory straight into LDS: lane L's 16 bytes land at
 // `lds` + 16 L (global_load_lds_dwordx4; M0 holds the wave-uniform LDS address, set one wait
