@@ -255,6 +255,30 @@ def test_ragged_tails_and_empty_prefix(lens):
     _check_case(c, what=f"tails {lens}")
 
 
+_BALANCED_LENS = [
+    # 32 sequences (the largest batch the balanced plan takes with 8 KV heads on 256 CUs): one long
+    # prefix among empty, sub-block, block-edge and page-edge lengths
+    [9000] + [0, 1, 31, 32, 33, 64, 65, 100, 511, 512, 513] * 2 + [7, 3, 2000, 4096, 0, 1, 15, 16, 17],
+    # one prefix long enough that its share of the items hits the per-sequence cap of 64 splits
+    [40000, 16],
+    # every prefix shorter than one block (the handle sized for 1024-token prefixes, so that its
+    # workspace holds the balanced plan's partials)
+    [1] * 16,
+]
+
+
+@pytest.mark.parametrize("lens", _BALANCED_LENS, ids=["b32_mixed", "b2_capped", "b16_tiny"])
+def test_balanced_schedule_extremes(lens):
+    """Length-balanced split schedule (computed on the device from the lengths): every sequence's
+    items, the per-sequence split cap, empty and sub-block prefixes, checked against the oracle."""
+    c = small(batch=len(lens), ctx_lens=lens, n_new=3, seed=37, max_pages_per_seq=max(64, -(-max(lens) // 16)))
+    with G.handle_for(c) as att:
+        pl = att.plan(c.batch, c.n_new, int(max(lens)))
+    # a balanced plan launches its items per KV head, independent of the batch (12 rows: one row tile)
+    assert pl["row_tiles"] == 1 and pl["workgroups"] == pl["splits"] * c.num_kv_heads, pl
+    _check_case(c, what=f"balanced {len(lens)} seqs, max {max(lens)}")
+
+
 @pytest.mark.parametrize("page_size", [32, 64, 128, 256])
 def test_page_sizes(page_size):
     c = small(ctx_lens=[700, 129, 3], page_size=page_size, seed=41)
