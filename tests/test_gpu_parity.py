@@ -217,6 +217,27 @@ def test_tall_tiles_outlier_keys(n_new, outliers):
     _check_case(c, what=f"tall tile n_new={n_new} outliers {no}x{sc:g}")
 
 
+@pytest.mark.parametrize("page_size", [32, 64, 256])
+def test_tall_tiles_page_sizes(page_size):
+    """256-row tiles (40 draft queries x 4 heads) on pages of 32 to 256 slots: both 16-key halves of
+    a block then sit in one page, and the prefix ends mid-page."""
+    c = small(n_new=40, max_draft=64, ctx_lens=[3000, 517, 0], page_size=page_size, seed=181)
+    with G.handle_for(c) as att:
+        assert att.plan(c.batch, c.n_new, 3000)["path"] == 3
+    _check_case(c, what=f"tall tile P={page_size}")
+
+
+@pytest.mark.parametrize("lens", [[0, 1, 31, 33, 100], [16, 32, 0, 5000, 64]])
+def test_tall_tree_short_prefixes(lens):
+    """60-node trees over prefixes of 0 to a few blocks: splits whose target range is empty, a last
+    split of draft blocks only, and a block ending mid-page, on the 256-row tile kernel."""
+    parents = np.stack([W.random_tree(191, b, 60) for b in range(len(lens))])
+    c = small(mode="tree", batch=len(lens), n_new=60, max_draft=64, parents=parents, ctx_lens=lens, seed=193)
+    with G.handle_for(c) as att:
+        assert att.plan(c.batch, c.n_new, int(max(lens)))["path"] == 3
+    _check_case(c, what=f"tall tree prefixes {lens}")
+
+
 @pytest.mark.parametrize("outliers", [(4, 8.0), (2, 32.0)])
 def test_tree_b8_ctx16k_n60_outlier_keys(outliers):
     no, sc = outliers
