@@ -76,7 +76,7 @@ kvshot_status kvshot_gated_delta_fusion_packed(kvshot_fusion_handle h, int32_t t
 
 /* Options: KVSHOT_OPT_SPLITS (0 automatic, else 1, 2, 4, 8 or 16 workgroups
  * along the reduction; capped by the workspace), KVSHOT_OPT_PATH (the token
- * tile: 0 automatic -- 128 tokens per workgroup for calls of 256 tokens or
+ * tile: 0 automatic -- 128 tokens per workgroup for calls of 128 tokens or
  * more, else 64; 1 always 64; 2 always 128, except with 8 or 16 forced
  * splits, which take 64) and KVSHOT_OPT_PROFILE (1: HIP events around each
  * kernel of every call), as for the attention handle.  Every plan computes the

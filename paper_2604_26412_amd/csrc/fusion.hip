@@ -128,6 +128,16 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
       ao[i] = load_o ? vo : u32x4{0u, 0u, 0u, 0u};
     }
   };
+  // one piece of the all-segment path, as loaded: n is zeroed for cross-only calls where it is
+  // staged (a select here would make the wave wait for the load)
+  auto load_a_piece = [&](int chunk, int i, u32x4 (&an)[kAPieces], u32x4 (&ao)[kAPieces]) {
+    const int pc = tid + 256 * i;
+    int m = m0 + pc / kRowPieces;
+    m = m < p.tokens ? m : p.tokens - 1;
+    const int64_t off = (int64_t)m * d + kbeg + chunk * kKC + 8 * (pc % kRowPieces);
+    an[i] = *(const u32x4*)(nsrc + off);
+    ao[i] = *(const u32x4*)(p.o + off);
+  };
   auto stage_a = [&](int buf, const u32x4 (&an)[kAPieces], const u32x4 (&ao)[kAPieces]) {
 #pragma unroll
     for (int i = 0; i < kAPieces; ++i) {
@@ -159,6 +169,10 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   for (int i = 0; i < NSEG; ++i)
     wpk[i] = p.w_packed + ((((int64_t)ntile * 4 + seg0 + i) * chunks_per_segment + kbeg / kKC) * 4 + w) * kSteps * 512 +
              lane * 8;
+  auto load_w_one = [&](int chunk, int i, int s, u32x4 (&dst)[NSEG][kSteps]) {
+    if constexpr (PACKED) dst[i][s] = *(const u32x4*)(wpk[i] + (int64_t)chunk * (4 * kSteps * 512) + s * 512);
+    else dst[i][s] = *(const u32x4*)(wrow[i] + kbeg + chunk * kKC + kHalfSpan * hh + 8 * s);
+  };
   auto load_w = [&](int chunk, u32x4 (&dst)[NSEG][kSteps]) {
     if constexpr (PACKED) {
 #pragma unroll
@@ -235,7 +249,140 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
     }
   };
 
-  // ---- main loop ----
+  u32x4 ran[PF][kAPieces], rao[PF][kAPieces];
+  u32x4 wreg[PF][NSEG][kSteps];
+  const int last = nchunks - 1;
+  if constexpr (NSEG == 4) {
+    // ---- main loop, software-pipelined (all four segments) ----
+    // Chunk c is computed in kSteps regions, one per MFMA k-step, from LDS
+    // buffer c & 1 and ring slot c % PF.  After each product the wave issues
+    // one small item, held in place by scheduling barriers, so that it goes
+    // out while the matrix core works through the product before it:
+    //  - the LDS read of the fragment that product has just freed, for the
+    //    next k-step (in the last region: chunk c + 1's first k-step, from the
+    //    other buffer, after the chunk's one barrier);
+    //  - one part of an activation piece of chunk c + 1 (its n and o written
+    //    to the other buffer, one word of its Delta formed, or its Delta
+    //    written), in the regions before the barrier;
+    //  - the global loads that refill the ring with chunk c + PF: in region
+    //    r the weights of k-step r - 1 (region 0: the previous slot's last
+    //    k-step), and piece i of the activations in the region after the
+    //    one that stages piece i of chunk c + 1 (whose registers that frees).
+    // Every item list is fixed at compile time, so the code of a chunk is one
+    // straight sequence.  Rows past the last token hold copies of the last
+    // token's row: their outputs are never stored, and no other row reads them.
+    constexpr int kNMF = 4 * kTB;                                   // products per region
+    constexpr int kStageRegions = kSteps - 1;                       // regions that stage (the last one has the barrier)
+    constexpr int kQ = 6;                                           // items per staged piece
+    bf16x8 f[kTB][3];
+    u32x4 dl[kAPieces];                                             // Delta of each piece, formed one word at a time
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      load_a(min(u, last), ran[u], rao[u]);
+      load_w(min(u, last), wreg[u]);
+    }
+    stage_a(0, ran[0], rao[0]);
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < kTB; ++t) {
+      const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh;
+#pragma unroll
+      for (int j = 0; j < 3; ++j) f[t][j] = as_bf16x8(*(const u32x4*)(&lds[0][j][0] + off));
+    }
+    // Nothing in flight on entry: otherwise the prologue's load order, merged with the loop's own at
+    // the loop head, makes the compiler wait for every load at the top of each iteration.
+    __builtin_amdgcn_s_waitcnt(0);
+    // chunk c from ring slot u = c % PF (u is a constant at every call)
+    auto chunk = [&](const int c, const int u) __attribute__((always_inline)) {
+      const int refill = min(c + PF, last);
+      const int refill_prev = min(c - 1 + PF, last);              // chunk c = 0: the data the slot already holds
+      u32x4 (&an1)[kAPieces] = ran[(u + 1) % PF];
+      u32x4 (&ao1)[kAPieces] = rao[(u + 1) % PF];
+      uint16_t* nbuf = &lds[(c + 1) & 1][0][0];
+      const uint16_t* cbuf = &lds[c & 1][0][0];
+#pragma unroll
+      for (int r = 0; r < kSteps; ++r) {
+        if (r == kSteps - 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          __syncthreads();                                        // chunk c + 1 staged; buffer c & 1 free after this region's reads
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        const uint16_t* rbase = r + 1 < kSteps ? cbuf : nbuf;
+        const int rs = r + 1 < kSteps ? r + 1 : 0;
+        // Items of region r, in order: the kQ parts of each piece staged in r (piece i is staged
+        // in region i kStageRegions / kAPieces: n and o written, Delta formed one word at a time,
+        // Delta written), the NSEG weight loads, and the loads of the slot's pieces whose
+        // counterparts were staged in the region before.  Item it follows product it kNMF / n_all.
+        int npc = 0, first_pc = 0, nld = 0, first_ld = 0;
+#pragma unroll
+        for (int i = 0; i < kAPieces; ++i) {
+          const int sr = (i * kStageRegions) / kAPieces;
+          if (sr == r) { first_pc = npc == 0 ? i : first_pc; ++npc; }
+          if (sr + 1 == r) { first_ld = nld == 0 ? i : first_ld; ++nld; }
+        }
+        const int n_all = kQ * npc + 4 + nld;
+#pragma unroll
+        for (int slot = 0; slot < kNMF; ++slot) {
+          const int t = slot >> 2, g = slot & 3;
+          // product g of block t: gate n, o, Delta; then the delta projection from Delta
+          if (g == 0) acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][0], as_bf16x8(wreg[u][0][r]), acc[0][t], 0, 0, 0);
+          if (g == 1) acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][1], as_bf16x8(wreg[u][1][r]), acc[0][t], 0, 0, 0);
+          if (g == 2) acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][2], as_bf16x8(wreg[u][2][r]), acc[0][t], 0, 0, 0);
+          if (g == 3) acc[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[t][2], as_bf16x8(wreg[u][3][r]), acc[1][t], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          // the fragment this product freed (Delta after its second use)
+          {
+            const int off = (32 * t + (lane & 31)) * kPitch + kHalfSpan * hh + 8 * rs;
+            if (g == 0) f[t][0] = as_bf16x8(*(const u32x4*)(rbase + off));
+            if (g == 1) f[t][1] = as_bf16x8(*(const u32x4*)(rbase + kTileElems + off));
+            if (g == 3) f[t][2] = as_bf16x8(*(const u32x4*)(rbase + 2 * kTileElems + off));
+          }
+          // this slot's share of the region's items
+          const int it_lo = (slot * n_all + kNMF - 1) / kNMF, it_hi = ((slot + 1) * n_all + kNMF - 1) / kNMF;
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            const int it = it_lo + k;
+            if (it >= it_hi) break;
+            if (it < kQ * npc) {
+              const int i = first_pc + it / kQ, q = it % kQ;
+              const int pc = tid + 256 * i;
+              uint16_t* dst = nbuf + (pc / kRowPieces) * kPitch + 8 * (pc % kRowPieces);
+              if (q == 0) {
+                an1[i] = load_n ? an1[i] : u32x4{0u, 0u, 0u, 0u};
+                *(u32x4*)dst = an1[i];
+                *(u32x4*)(dst + kTileElems) = ao1[i];
+              } else if (q < kQ - 1) {
+                const int e = q - 1;                                // o - n per bf16 element (exact in float32), rounded to bf16
+                dl[i][e] = pack_bf16x2(bf16_lo(ao1[i][e]) - bf16_lo(an1[i][e]), bf16_hi(ao1[i][e]) - bf16_hi(an1[i][e]));
+              } else {
+                *(u32x4*)(dst + 2 * kTileElems) = dl[i];
+              }
+            } else if (it < kQ * npc + 4) {
+              const int sg = it - kQ * npc;
+              if (r > 0) load_w_one(refill, sg, r - 1, wreg[u]);
+              else load_w_one(refill_prev, sg, kSteps - 1, wreg[(u + PF - 1) % PF]);
+            } else {
+              load_a_piece(refill, first_ld + (it - kQ * npc - 4), ran[u], rao[u]);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // the last region's weights are refilled in the next chunk's first region
+    };
+    // Whole ring groups in the loop and the rest after it: a chunk skipped inside the loop would
+    // leave different loads in flight on one path into the loop head, and the compiler would then
+    // wait for every load there.
+    int c0 = 0;
+    for (; c0 + PF <= nchunks; c0 += PF) {
+#pragma unroll
+      for (int u = 0; u < PF; ++u) chunk(c0 + u, u);
+    }
+#pragma unroll
+    for (int u = 0; u + 1 < PF; ++u)
+      if (c0 + u < nchunks) chunk(c0 + u, u);
+  } else {
+  // ---- main loop of the split kernels ----
   // Ring slot c % PF holds the activation and weight registers of chunk c.
   // Chunk c is computed from LDS buffer c & 1 and its weight slot; then the
   // activations of chunk c + 1 go to the other buffer, and the slot is
@@ -243,9 +390,6 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
   // chunk; iterations past the last chunk only keep the pattern), so the
   // loads behind each slot are the same on every path and the waits cover
   // just the slot in use.
-  u32x4 ran[PF][kAPieces], rao[PF][kAPieces];
-  u32x4 wreg[PF][NSEG][kSteps];
-  const int last = nchunks - 1;
 #pragma unroll
   for (int u = 0; u < PF; ++u) {
     load_a(min(u, last), ran[u], rao[u]);
@@ -269,6 +413,7 @@ __global__ __launch_bounds__(256, WPS) void fusion_kernel(FusionParams p) {
       load_w(min(c + PF, last), wreg[u]);
       __syncthreads();
     }
+  }
   }
 
   // ---- epilogue: accumulator register v of lane (channel, hh) is token 8(v/4) + 4hh + v%4 of its 32-row tile ----
@@ -352,7 +497,7 @@ __global__ __launch_bounds__(256) void fusion_combine_kernel(FusionParams p) {
 #endif
 
 #ifndef KVSHOT_FUSION_PF4_TT128
-#define KVSHOT_FUSION_PF4_TT128 3
+#define KVSHOT_FUSION_PF4_TT128 2
 #endif
 
 template <bool PACKED>

@@ -40,7 +40,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 int m_tiles_of(int tokens, int tile = kFusionTokens) { return (tokens + tile - 1) / tile; }
 
 // Automatic plans consider 128-token tiles from this many tokens.
-constexpr int kFusionBigTileMin = 256;
+constexpr int kFusionBigTileMin = 128;
 
 // The plan of a call: token tile, reduction splits and how a split divides the
 // reduction space.
@@ -57,9 +57,10 @@ constexpr int kFusionBigTileMin = 256;
 //    CU (a 128-token workgroup holds a CU's registers); a split takes a part of
 //    the reduction index range of all four segments, so it reads only that
 //    part of n and o.  Automatic plans take them from kFusionBigTileMin tokens
-//    on.  Measured at d = 4096 (main kernel + combine, 64 -> 128-token tiles):
-//    256 tokens 75 -> 65 us, 384 tokens 97 -> 97 us, 480 tokens 107 -> 98 us,
-//    640 to 1024 tokens 216 -> 178 us.
+//    on.  Measured at d = 4096 (main kernel + combine, graph replay, 64 ->
+//    128-token tiles): 128 tokens 53 -> 46 us, 192 tokens 71 -> 52 us, 256
+//    tokens 75 -> 53 us, 384 tokens 98 -> 71 us, 480 tokens 109 -> 83 us, 640
+//    tokens 150 -> 120 us, 1024 tokens 172 -> 154 us.
 // Both capped by the workspace.
 struct FusionPlan {
   int tile = kFusionTokens, splits = 1, kparts = 1, m_tiles = 0;

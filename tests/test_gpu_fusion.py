@@ -82,12 +82,14 @@ def test_fusion_matches_oracle(tokens, d, splits):
     assert np.max(np.abs(g - g_ref)) <= 5e-3
 
 
-@pytest.mark.parametrize("d", [256, 512])
+@pytest.mark.parametrize("d", [256, 512, 768])
 @pytest.mark.parametrize("tokens", [1, 100, 128, 200, 300])
 @pytest.mark.parametrize("splits", [0, 1, 2, 4])
 def test_fusion_128_token_tiles_match_oracle(tokens, d, splits):
     # 128-token tiles (KVSHOT_OPT_PATH 2): splits take parts of the reduction index range of all four
-    # segments; ragged last tiles at 100, 200 and 300 tokens
+    # segments; ragged last tiles at 100, 200 and 300 tokens.  The main loop runs whole pairs of
+    # 64-index chunks and then the rest: d = 256 with 4 splits has one chunk per split (no pair),
+    # d = 768 with 4 splits three (one pair and one more)
     from paper_2604_26412_amd import GatedDeltaFusion, OPT_SPLITS, OPT_PATH
     _log(f"fusion 128-token tiles tokens={tokens} d={d} splits={splits}")
     c = W.fusion_case(tokens, d, seed=tokens * 11 + d + splits)
@@ -102,7 +104,7 @@ def test_fusion_128_token_tiles_match_oracle(tokens, d, splits):
     assert np.max(np.abs(g - g_ref)) <= 5e-3
 
 
-@pytest.mark.parametrize("tokens", [256, 300, 480])
+@pytest.mark.parametrize("tokens", [128, 200, 256, 300, 480])
 def test_fusion_automatic_plan_at_large_token_counts(tokens):
     from paper_2604_26412_amd import GatedDeltaFusion
     c = W.fusion_case(tokens, 512, seed=tokens + 3)
