@@ -189,13 +189,28 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
     const uint16_t* x;    // the chunk's head-half of the source layer
     uint16_t* lds;        // the stage
   };
-  auto target = [&](int c, int stage) {
-    const int k0 = k_first + c * KC;
-    const int l = k0 / d_kv;
-    const int rem = k0 - l * d_kv;
+  // Cursor on the chunk whose loads are issued next: chunk cur_c starts at reduction index
+  // k_first + cur_c KC, offset cur_rem into source layer cur_l.  It moves one chunk at a time and
+  // stops at the last chunk; the layer's pool pointer is read from LDS again only when a chunk
+  // starts a new layer (a chunk never straddles one), so no chunk waits on that read or divides.
+  int cur_c = 0, cur_l = k_first / d_kv;
+  int cur_rem = k_first - cur_l * d_kv;
+  const uint16_t* cur_pool = t_layer[g][cur_l];
+  auto advance = [&]() {
+    if (cur_c + 1 < nch) {
+      ++cur_c;
+      cur_rem += KC;
+      if (cur_rem == d_kv) {
+        cur_rem = 0;
+        ++cur_l;
+        cur_pool = t_layer[g][cur_l];
+      }
+    }
+  };
+  auto target = [&](int stage) {
     Target t;
-    t.w = wsrc + k0;
-    t.x = t_layer[g][l] + (int64_t)(rem >> 7) * p.head_stride + (rem & 127);
+    t.w = wsrc + k_first + cur_c * KC;
+    t.x = cur_pool + (int64_t)(cur_rem >> 7) * p.head_stride + (cur_rem & 127);
     t.lds = smem + stage * 2 * kStageElems + (kLoads * w) * 512;
     return t;
   };
@@ -219,23 +234,36 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
 #pragma unroll
   for (int st = 0; st < kSteps; ++st) frag_off[st] = 8 * ((hh * kSteps + st) ^ swz);
   static_assert(2 * kLoads == 4 * kSteps, "one load per four MFMAs");
-  // One chunk from `stage`, with the loads of a later chunk (`nt`) issued one per four MFMAs (so
-  // no wave stalls on a burst of load issues before its first MFMA) and the next k-step's
-  // fragments read during the current one.  The order is pinned with scheduling barriers.
-  auto compute = [&](int stage, const Target& nt) {
+  static_assert(NS >= 3, "the next chunk is read while a later one is still in flight");
+  // Fragments of one k-step, double-buffered across k-steps and across chunks.
+  bf16x8 a[2][4], b[2][4];
+  auto read = [&](int stage, int st, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
     const uint16_t* A = smem + stage * 2 * kStageElems + (128 * wc + (lane & 31)) * KC;
     const uint16_t* B = smem + stage * 2 * kStageElems + kStageElems + (128 * wt + (lane & 31)) * KC;
-    bf16x8 a[2][4], b[2][4];
-    auto read = [&](int st, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = as_bf16x8(*(const u32x4*)(A + 32 * i * KC + frag_off[st]));
+    for (int i = 0; i < 4; ++i) fa[i] = as_bf16x8(*(const u32x4*)(A + 32 * i * KC + frag_off[st]));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = as_bf16x8(*(const u32x4*)(B + 32 * j * KC + frag_off[st]));
-    };
-    read(0, a[0], b[0]);
+    for (int j = 0; j < 4; ++j) fb[j] = as_bf16x8(*(const u32x4*)(B + 32 * j * KC + frag_off[st]));
+  };
+  // Chunk c from `stage` (its first k-step's fragments already read), with the loads of a later
+  // chunk (`nt`) issued one per four MFMAs (so no wave stalls on a burst of load issues before its
+  // first MFMA) and the next k-step's fragments read during the current one -- in the last k-step,
+  // those of chunk c + 1's first k-step from `next_stage`.  The chunk's one barrier sits before
+  // its last k-step: by then every wave has its share of chunk c + 1 in LDS (the wait before the
+  // barrier) and has finished reading chunk c - 1, whose stage the loads refill; so the first
+  // reads of the next chunk no longer wait behind a barrier with nothing to compute.  The order is
+  // pinned with scheduling barriers.
+  auto compute = [&](int stage, int next_stage, const Target& nt) {
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
-      if (st + 1 < kSteps) read(st + 1, a[(st + 1) & 1], b[(st + 1) & 1]);
+      if (st + 1 == kSteps) {
+        // in flight may stay: the NS - 3 chunks after c + 1 and this chunk's loads so far
+        wait_vmcnt<(NS - 3) * 2 * kLoads + 4 * (kSteps - 1)>();
+        lds_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (st + 1 < kSteps) read(stage, st + 1, a[(st + 1) & 1], b[(st + 1) & 1]);
+      else read(next_stage, 0, a[(st + 1) & 1], b[(st + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -247,24 +275,29 @@ __global__ __launch_bounds__(256, 1) void kvproj_kernel(KvProjParams p) {
       }
     }
   };
+  static_assert(kSteps % 2 == 0, "a chunk's first k-step uses fragment buffer 0");
 
-  // ---- main loop.  Chunks 0 .. NS - 2 are issued up front; iteration c waits for chunk c (the
-  // NS - 2 younger chunks may stay in flight), passes a barrier (every wave is then done with
-  // chunk c - 1, so its stage is free) and computes c while issuing chunk c + NS - 1 into that
-  // stage.  Loads past the last chunk re-read it into a stage nobody reads again. ----
+  // ---- main loop.  Chunks 0 .. NS - 2 are issued up front, chunk 0 is waited for and its first
+  // k-step read; iteration c computes c from stage c % NS while issuing chunk c + NS - 1 into the
+  // stage of chunk c - 1 (free: every wave finished reading it before chunk c - 1's barrier).
+  // Loads past the last chunk re-read it into a stage nobody reads again, and the last chunk's
+  // reads of "the next chunk" read a stage whose values are never used. ----
 #pragma unroll
   for (int c = 0; c < NS - 1; ++c) {
-    const Target t = target(c < nch ? c : nch - 1, c);
+    const Target t = target(c);
 #pragma unroll
     for (int idx = 0; idx < 2 * kLoads; ++idx) issue_one(t, idx);
+    advance();
   }
+  wait_vmcnt<(NS - 2) * 2 * kLoads>();
+  lds_barrier();
+  read(0, 0, a[0], b[0]);
   int stage = 0;
   for (int c = 0; c < nch; ++c) {
-    wait_vmcnt<(NS - 2) * 2 * kLoads>();
-    lds_barrier();
-    const int nxt = c + NS - 1;
-    compute(stage, target(nxt < nch ? nxt : nch - 1, stage == 0 ? NS - 1 : stage - 1));
-    stage = stage == NS - 1 ? 0 : stage + 1;
+    const int next_stage = stage == NS - 1 ? 0 : stage + 1;
+    compute(stage, next_stage, target(stage == 0 ? NS - 1 : stage - 1));   // the cursor is at chunk c + NS - 1 (clamped)
+    advance();
+    stage = next_stage;
   }
   wait_vmcnt<0>();     // the trailing re-reads land before the workgroup ends
 
