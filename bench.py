@@ -192,6 +192,32 @@ def stream_ceiling(torch, K, tensor):
     return tensor.numel() * tensor.element_size() / (e0.elapsed_time(e1) / 10 * 1e-3) / 1e9
 
 
+def mfma_ceiling(torch, K, iters: int = 4096):
+    """Dense bf16 matrix rate the whole chip sustains (TFLOP/s): ten back-to-back launches of the
+    library's matrix-rate probe, about 1 ms each, one workgroup of four waves per CU."""
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.empty(wgs * 4, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        K.mfma_rate(iters, wgs, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        K.mfma_rate(iters, wgs, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    flops = wgs * 4 * iters * 16 * 32768.0
+    return flops / (e0.elapsed_time(e1) / 10 * 1e-3) / 1e12
+
+
+def add_mfma_ceiling(torch, K, roof):
+    """For a matrix-bound kernel, the measured sustained matrix rate beside the published peak."""
+    if roof["bound"] != "mfma":
+        return
+    ceil = mfma_ceiling(torch, K)
+    roof["measured_mfma_ceiling"] = round(ceil, 1)
+    roof["frac_of_measured_ceiling"] = round(roof["achieved"] / ceil, 4)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -580,6 +606,7 @@ def bench_fusion(args, torch, K, W):
         roof = {"bound": "hbm", "achieved": round(main_bytes / (main_ms * 1e-3) / 1e9, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    add_mfma_ceiling(torch, K, roof)
     roof["traffic"] = read_fusion_traffic(name) if not (args.splits or args.fusion_tile) else None
     roof.update({"kernel": f"fusion_kernel ({plan['splits']} reduction split(s), {plan['workgroups']} workgroups)",
                  "kernel_ms": round(main_ms, 5), "combine_ms": round(comb_ms, 5),
@@ -824,6 +851,7 @@ def bench_kvproj(args, torch, K, W):
     else:
         roof = {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    add_mfma_ceiling(torch, K, roof)
     kfile = "kvproj_direct_kernel" if plan["path"] == 2 else "kvproj_kernel"
     roof["traffic"] = read_kvproj_traffic(name, kfile) if not (args.splits or args.no_rope or args.kvproj_path) else None
     if plan["path"] == 2:

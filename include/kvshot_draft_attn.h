@@ -250,6 +250,17 @@ kvshot_status kvshot_debug_tree_mask(kvshot_handle h, int32_t batch, int32_t n_n
  * bytes).  Times the device's practical streaming-read bandwidth. */
 kvshot_status kvshot_debug_stream_read(const void* src, int64_t bytes, void* sink, int32_t sink_words, void* stream);
 
+/* Measurement helper: `workgroups` workgroups of four waves (one per SIMD of a
+ * CU) each issue `iters` x 16 dense bf16 32x32x16 matrix products per wave,
+ * with no memory traffic; each workgroup writes one 16-byte word of `sink`
+ * (device, >= 16*workgroups bytes).  A launch performs workgroups x 4 x iters
+ * x 16 x 32768 flops.  Times the rate the matrix cores sustain when every SIMD
+ * runs them (the clock the chip holds under that load included), the
+ * counterpart of the streaming-read probe for matrix-bound kernels.
+ * Returns KVSHOT_ERR_INVALID_ARG for workgroups or iters below 1 or a null or
+ * unaligned sink. */
+kvshot_status kvshot_debug_mfma_rate(int32_t workgroups, int32_t iters, void* sink, void* stream);
+
 /* Static text for a status code. */
 const char* kvshot_status_string(int32_t status);
 

@@ -29,7 +29,7 @@ EXPORTED_SYMBOLS = [
     "kvshot_draft_attn_init", "kvshot_draft_attn_destroy", "kvshot_draft_attn_step", "kvshot_draft_attn_tree",
     "kvshot_draft_attn_validate", "kvshot_draft_attn_set_option", "kvshot_draft_attn_plan",
     "kvshot_draft_attn_profile_read", "kvshot_debug_gather_kv", "kvshot_debug_tree_mask", "kvshot_debug_stream_read",
-    "kvshot_status_string", "kvshot_draft_attn_call", "kvshot_draft_attn_call_noalloc",
+    "kvshot_debug_mfma_rate", "kvshot_status_string", "kvshot_draft_attn_call", "kvshot_draft_attn_call_noalloc",
     "kvshot_draft_attn_validate_call",
     "kvshot_fusion_init", "kvshot_fusion_destroy", "kvshot_gated_delta_fusion", "kvshot_fusion_set_option",
     "kvshot_fusion_plan", "kvshot_fusion_profile_read", "kvshot_fusion_pack_weights",
@@ -114,6 +114,7 @@ def load_library(path: Optional[str] = None):
         "kvshot_debug_gather_kv": [_vp, _i32, _i32] + [_vp] * 7,
         "kvshot_debug_tree_mask": [_vp, _i32, _i32, _vp, _vp, _vp, _vp],
         "kvshot_debug_stream_read": [_vp, _i64, _vp, _i32, _vp],
+        "kvshot_debug_mfma_rate": [_i32, _i32, _vp, _vp],
         "kvshot_draft_attn_call": [_vp, ctypes.POINTER(KvshotCall), _vp],
         "kvshot_draft_attn_call_noalloc": [_vp, ctypes.POINTER(KvshotCall), _vp],
         "kvshot_draft_attn_validate_call": [_vp, ctypes.POINTER(KvshotCall), ctypes.POINTER(_i32), _vp],
@@ -184,6 +185,19 @@ def stream_read(src, sink=None, workgroups: int = 2048, stream=None):
     st = lib.kvshot_debug_stream_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(), workgroups,
                                       stream if stream is not None else torch.cuda.current_stream().cuda_stream)
     _check("kvshot_debug_stream_read", st)
+    return sink
+
+
+def mfma_rate(iters: int, workgroups: int = 256, sink=None, stream=None):
+    """Dense bf16 matrix work with no memory traffic (matrix-rate probe); returns the sink.
+    One launch performs workgroups x 4 x iters x 16 x 32768 flops."""
+    torch = _torch()
+    lib = load_library()
+    if sink is None:
+        sink = torch.empty(workgroups * 4, dtype=torch.int32, device="cuda")
+    st = lib.kvshot_debug_mfma_rate(workgroups, iters, sink.data_ptr(),
+                                    stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+    _check("kvshot_debug_mfma_rate", st)
     return sink
 
 

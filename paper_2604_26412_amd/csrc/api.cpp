@@ -17,6 +17,11 @@
 #include "device_guard.h"
 #include "kvshot_common.h"
 
+namespace kvshot {
+// the matrix-rate probe (csrc/debug.hip); declared here, beside its one caller
+hipError_t launch_mfma_rate(int blocks, int iters, void* sink, hipStream_t s);
+}  // namespace kvshot
+
 using namespace kvshot;
 
 namespace {
@@ -732,6 +737,12 @@ kvshot_status kvshot_debug_stream_read(const void* src, int64_t bytes, void* sin
   if (!src || !sink || bytes < 16 || sink_words < 1 || !aligned16(src) || !aligned16(sink))
     return KVSHOT_ERR_INVALID_ARG;
   if (launch_stream_read(src, bytes, sink, sink_words, (hipStream_t)stream) != hipSuccess) return KVSHOT_ERR_DEVICE;
+  return KVSHOT_OK;
+}
+
+kvshot_status kvshot_debug_mfma_rate(int32_t workgroups, int32_t iters, void* sink, void* stream) {
+  if (workgroups < 1 || iters < 1 || !sink || !aligned16(sink)) return KVSHOT_ERR_INVALID_ARG;
+  if (launch_mfma_rate(workgroups, iters, sink, (hipStream_t)stream) != hipSuccess) return KVSHOT_ERR_DEVICE;
   return KVSHOT_OK;
 }
 

@@ -111,7 +111,51 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const sr_u32x4* __rest
   }
 }
 
+// Dense bf16 matrix work with no memory traffic: every wave issues iters x 16
+// 32x32x16 products into four accumulators in turn, and each workgroup stores
+// one word so the products cannot be dropped.  One workgroup of four waves per
+// CU (one wave per SIMD).  Used only to measure the rate the matrix cores
+// sustain when every SIMD runs them.
+typedef __bf16 mr_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float mr_f32x16 __attribute__((ext_vector_type(16)));
+__global__ __launch_bounds__(256, 1) void mfma_rate_kernel(int iters, sr_u32x4* sink) {
+  const int lane = threadIdx.x & 63;
+  mr_bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (float)(lane + i));
+    b[i] = (__bf16)(0.002f * (float)(lane - i));
+  }
+  mr_f32x16 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = mr_f32x16{};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[j][e];
+  __shared__ uint32_t red[256];
+  red[threadIdx.x] = __float_as_uint(s);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t r = 0;
+    for (int k = 0; k < 256; ++k) r ^= red[k];
+    sink[blockIdx.x] = sr_u32x4{r, 0u, 0u, 0u};
+  }
+}
+
 }  // namespace
+
+hipError_t launch_mfma_rate(int blocks, int iters, void* sink, hipStream_t s) {
+  hipLaunchKernelGGL(mfma_rate_kernel, dim3(blocks), dim3(256), 0, s, iters, (sr_u32x4*)sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int blocks, hipStream_t s) {
   hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(256), 0, s, (const sr_u32x4*)src, bytes / 16,

@@ -172,6 +172,10 @@ static void attention() {
   EXPECT(kvshot_debug_gather_kv(h, 2, 256, dev(), dev(), (const int32_t*)dev(), (const int32_t*)dev(), dev(), dev(),
                                 nullptr) == KVSHOT_OK);
   EXPECT(kvshot_debug_stream_read(dev(), 1 << 20, dev(), 256, nullptr) == KVSHOT_OK);
+  EXPECT(kvshot_debug_mfma_rate(256, 16, dev(), nullptr) == KVSHOT_OK);
+  EXPECT(kvshot_debug_mfma_rate(0, 16, dev(), nullptr) == KVSHOT_ERR_INVALID_ARG);
+  EXPECT(kvshot_debug_mfma_rate(256, 0, dev(), nullptr) == KVSHOT_ERR_INVALID_ARG);
+  EXPECT(kvshot_debug_mfma_rate(256, 16, nullptr, nullptr) == KVSHOT_ERR_INVALID_ARG);
   for (int s = 0; s <= 7; ++s) EXPECT(kvshot_status_string(s) != nullptr);
   EXPECT(kvshot_draft_attn_destroy(h) == KVSHOT_OK);
   EXPECT(kvshot_draft_attn_destroy(nullptr) == KVSHOT_OK);

@@ -144,6 +144,11 @@ hipError_t launch_stream_read(const void* src, int64_t bytes, void* sink, int bl
   ++g_launches;
   return hipSuccess;
 }
+hipError_t launch_mfma_rate(int blocks, int iters, void* sink, hipStream_t) {
+  need(sink && blocks > 0 && iters > 0, "mfma rate");
+  ++g_launches;
+  return hipSuccess;
+}
 hipError_t launch_fusion(const FusionParams& p, hipStream_t) {
   need(p.tile_tokens == 64 || p.tile_tokens == 128, "fusion tile");
   need(p.m_tiles * p.tile_tokens >= p.tokens && (p.m_tiles - 1) * p.tile_tokens < p.tokens, "fusion token tiles");

@@ -87,6 +87,8 @@ def test_null_arguments(lib):
     assert lib.kvshot_draft_attn_profile_read(None, None, None, None) == 1
     assert lib.kvshot_debug_tree_mask(None, 1, 1, None, None, None, None) == 1
     assert lib.kvshot_debug_gather_kv(None, 1, 1, *([None] * 7)) == 1
+    assert lib.kvshot_debug_mfma_rate(0, 1, None, None) == 1
+    assert lib.kvshot_debug_mfma_rate(1, 0, None, None) == 1
     assert lib.kvshot_draft_attn_validate(None, 1, 1, 16, None, None, None, None, None, None) == 1
     assert lib.kvshot_draft_attn_destroy(None) == 0
 
